@@ -1,0 +1,353 @@
+"""Pins of the CPU oracle against things other than itself (CPU only).
+
+* brute force on tiny inputs (tests/bruteforce.py, scalar loops);
+* library special cases (torch CPU: softmax attention, norms, activations,
+  pixel (un)shuffle) -- the oracle uses none of these routines itself;
+* the worked example of Fig. 2(a) (W_frm = 2, three latent frames);
+* invariants: streaming == full masked pass (Sec. 3.3), causality, RoPE
+  relative-position property, reductions W >= T' and W = 1;
+* closed forms: parameter counts of Table 5, KV-cache shape of Eq. kv_cache.
+"""
+import copy
+from dataclasses import replace
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as Fnn
+
+import oracle.decoder as od
+from oracle import (attention, apply_rope, band_mask, decode_full, decode_stream,
+                    gelu, layer_norm, pixel_shuffle_frame, pixel_unshuffle_frame,
+                    rms_norm, rope_angles, silu, StreamingOracle)
+from paper_2607_14898_amd.workloads import (MODELS, ModelConfig, make_latents, make_weights,
+                                            param_count, round_to_bf16)
+from tests import bruteforce
+
+# micro decoders small enough for the scalar brute force
+MICRO = ModelConfig(
+    compute_dtype="f32", latent_channels=2, latent_h=4, latent_w=4, patch=2,
+    dim=32, n_heads=2, n_kv_groups=1, n_backbone_blocks=1, n_refine_blocks=1,
+    mlp_hidden=32, head_hidden=16, r_t=2, s_out=2, window=2)
+MICRO_ASIS = replace(MICRO, n_kv_groups=2, n_refine_blocks=0, mlp_kind="gelu",
+                     norm_kind="ln", head_kind="linear", kv_norm=False, rope=False,
+                     norm_eps=1e-5, window=1, unit_frames=2, patch=1, latent_h=2,
+                     latent_w=2, clamp_output=False)
+MICRO_MIX = replace(MICRO, n_heads=4, n_kv_groups=2, dim=64, mlp_kind="gelu",
+                    n_backbone_blocks=2, window=1, clamp_output=False)
+
+
+def _micro_inputs(cfg, frames=3, seed=7):
+    W = make_weights(cfg, seed, std=0.3)
+    z = make_latents(cfg, frames, seed + 1)[0]
+    return W, z
+
+
+def _bf_array(cfg, W, z):
+    return np.array(bruteforce.decode(cfg, W, z), dtype=np.float64)
+
+
+# ----------------------------------------------------------------- whole decoder
+
+@pytest.mark.parametrize("cfg", [MICRO, MICRO_ASIS, MICRO_MIX], ids=["paper", "asis", "mix"])
+def test_whole_decoder_matches_bruteforce(cfg):
+    W, z = _micro_inputs(cfg, frames=4 if cfg.unit_frames == 2 else 3)
+    ref = _bf_array(cfg, W, z)
+    got_full = decode_full(cfg, W, z)
+    got_stream = decode_stream(cfg, W, z[None], cfg.unit_frames)[0]
+    assert ref.shape == got_full.shape == got_stream.shape
+    # the test is only meaningful if outputs are not all clamped or all tiny
+    assert 0.05 < np.std(ref) and np.mean(np.abs(ref) == 1.0) < 0.5
+    np.testing.assert_allclose(got_full, ref, atol=1e-12, rtol=0)
+    np.testing.assert_allclose(got_stream, ref, atol=1e-12, rtol=0)
+
+
+MUTATIONS = {
+    "drop_o_bias": lambda: _patch_block_post(drop="bo"),
+    "silu_as_sigmoid": lambda: setattr(od, "silu", lambda x: 1.0 / (1.0 + np.exp(-x))),
+    "rope_sign": lambda: setattr(od, "apply_rope", lambda x, a: _ORIG["apply_rope"](x, -a)),
+    "tup_order": lambda: setattr(od, "_temporal_up", _tup_wrong),
+    "shuffle_swap": lambda: setattr(od, "pixel_shuffle_frame", _shuffle_wrong),
+    "gqa_interleave": lambda: setattr(od, "attention", _attn_interleaved),
+    "rms_no_gain": lambda: setattr(od, "rms_norm", lambda x, g, e: _ORIG["rms_norm"](x, 1.0, e)),
+    "unshuffle_swap": lambda: setattr(od, "pixel_unshuffle_frame", _unshuffle_wrong),
+}
+_ORIG = {k: getattr(od, k) for k in ("silu", "apply_rope", "_temporal_up", "pixel_shuffle_frame",
+                                     "attention", "rms_norm", "_block_post_attention",
+                                     "pixel_unshuffle_frame")}
+
+
+def _patch_block_post(drop):
+    def f(cfg, W, p, x, o):
+        W2 = dict(W)
+        W2[p + "." + drop] = np.zeros_like(W[p + "." + drop])
+        return _ORIG["_block_post_attention"](cfg, W2, p, x, o)
+    od._block_post_attention = f
+
+
+def _tup_wrong(cfg, W, y, frames):
+    L, D, r = cfg.tokens_per_frame, cfg.dim, cfg.r_t
+    t = y @ W["tup.w"].T + W["tup.b"]
+    t = t.reshape(frames, L, D, r).transpose(0, 3, 1, 2)   # channel d r + j instead of j D + d
+    return t.reshape(frames * r * L, D)
+
+
+def _shuffle_wrong(f, gh, gw, s, c):
+    a = f.reshape(gh, gw, c, s, s).transpose(2, 0, 4, 1, 3)
+    return a.reshape(c, gh * s, gw * s)
+
+
+def _unshuffle_wrong(zf, p):
+    C, H, W = zf.shape
+    a = zf.reshape(C, H // p, p, W // p, p).transpose(1, 3, 0, 4, 2)
+    return a.reshape((H // p) * (W // p), C * p * p)
+
+
+def _attn_interleaved(q, k, v, mask=None, return_probs=False):
+    N, G = q.shape[1], k.shape[1]
+    kk = k[:, [n % G for n in range(N)], :]
+    vv = v[:, [n % G for n in range(N)], :]
+    return _ORIG["attention"](q, kk, vv, mask, return_probs)
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_planted_oracle_mistakes_are_caught(name):
+    """A plausible mistake planted in the oracle must break the brute-force pin."""
+    cfg = replace(MICRO, n_heads=4, n_kv_groups=2, dim=64)
+    W, z = _micro_inputs(cfg)
+    ref = _bf_array(cfg, W, z)
+    saved = {k: getattr(od, k) for k in _ORIG}
+    try:
+        MUTATIONS[name]()
+        got = decode_full(cfg, W, z)
+    finally:
+        for k, f in saved.items():
+            setattr(od, k, f)
+    assert np.max(np.abs(got - ref)) > 1e-4
+
+
+# ----------------------------------------------------------------- attention
+
+def _brute_attention(q, k, v, visible):
+    Lq, N, Dh = q.shape
+    G = k.shape[1]
+    out = np.zeros((Lq, N, Dh))
+    for i in range(Lq):
+        for n in range(N):
+            g = (n * G) // N
+            keys = [j for j in range(k.shape[0]) if visible[i][j]]
+            sc = [float(np.dot(q[i, n], k[j, g])) / np.sqrt(Dh) for j in keys]
+            m = max(sc)
+            e = [np.exp(s - m) for s in sc]
+            for t, j in enumerate(keys):
+                out[i, n] += e[t] / sum(e) * v[j, g]
+    return out.reshape(Lq, N * Dh)
+
+
+def test_attention_brute_force_and_softmax_rows():
+    rng = np.random.default_rng(3)
+    q = rng.standard_normal((6, 4, 8)) * 2
+    k = rng.standard_normal((9, 2, 8))
+    v = rng.standard_normal((9, 2, 8))
+    vis = band_mask(np.array([0, 0, 1, 1, 2, 2]), np.array([0, 0, 0, 1, 1, 1, 2, 2, 2]), 2)
+    o, probs = attention(q, k, v, vis, return_probs=True)
+    np.testing.assert_allclose(o, _brute_attention(q, k, v, vis), atol=1e-12, rtol=0)
+    np.testing.assert_allclose(probs.sum(-1), 1.0, atol=1e-12, rtol=0)
+    assert np.all(probs[:, ~vis] == 0.0)
+
+
+def test_attention_matches_torch_sdpa_and_gqa_reductions():
+    rng = np.random.default_rng(4)
+    N, G, Dh = 8, 2, 16
+    q = rng.standard_normal((20, N, Dh))
+    k = rng.standard_normal((30, G, Dh))
+    v = rng.standard_normal((30, G, Dh))
+    o = attention(q, k, v)
+    # library: torch SDPA with K/V heads repeated N/G times (GQA == MHA with repeats)
+    rep = np.repeat(np.arange(G), N // G)
+    tq = torch.from_numpy(q).permute(1, 0, 2)
+    tk = torch.from_numpy(k[:, rep]).permute(1, 0, 2)
+    tv = torch.from_numpy(v[:, rep]).permute(1, 0, 2)
+    ref = Fnn.scaled_dot_product_attention(tq, tk, tv).permute(1, 0, 2).reshape(20, N * Dh)
+    np.testing.assert_allclose(o, ref.numpy(), atol=1e-12, rtol=0)
+    # G == N is plain multi-head attention
+    o2 = attention(q, k[:, rep], v[:, rep])
+    np.testing.assert_allclose(o, o2, atol=1e-13, rtol=0)
+
+
+# ----------------------------------------------------------------- elementwise
+
+def test_norms_and_activations_match_torch():
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((7, 48)) * 3
+    g = 1 + 0.1 * rng.standard_normal(48)
+    b = 0.1 * rng.standard_normal(48)
+    tx = torch.from_numpy(x)
+    np.testing.assert_allclose(
+        rms_norm(x, g, 1e-6), Fnn.rms_norm(tx, (48,), torch.from_numpy(g), 1e-6).numpy(),
+        atol=1e-13, rtol=0)
+    np.testing.assert_allclose(
+        layer_norm(x, g, b, 1e-5),
+        Fnn.layer_norm(tx, (48,), torch.from_numpy(g), torch.from_numpy(b), 1e-5).numpy(),
+        atol=1e-13, rtol=0)
+    np.testing.assert_allclose(silu(x), Fnn.silu(tx).numpy(), atol=1e-14, rtol=0)
+    np.testing.assert_allclose(gelu(x), Fnn.gelu(tx).numpy(), atol=1e-14, rtol=0)
+
+
+# ----------------------------------------------------------------- RoPE
+
+def test_rope_properties():
+    rng = np.random.default_rng(6)
+    Dh = 64
+    x = rng.standard_normal((5, 3, Dh))
+    y = rng.standard_normal((5, 3, Dh))
+    pos = rng.integers(0, 50, size=(5, 3)).astype(float)
+    xr = apply_rope(x, rope_angles(pos, Dh, 1e4))
+    # rotation preserves norms; position zero is the identity
+    np.testing.assert_allclose(np.linalg.norm(xr, axis=-1), np.linalg.norm(x, axis=-1), rtol=1e-13)
+    np.testing.assert_allclose(apply_rope(x, rope_angles(np.zeros((5, 3)), Dh, 1e4)), x, atol=0)
+    # scores depend on the position difference only (per axis)
+    d = rng.integers(-20, 20, size=(5, 3)).astype(float)
+    shift = np.array([[1000.0, 7.0, -3.0]])
+    s1 = np.sum(apply_rope(x, rope_angles(pos, Dh, 1e4)) *
+                apply_rope(y, rope_angles(pos + d, Dh, 1e4)), axis=-1)
+    s2 = np.sum(apply_rope(x, rope_angles(pos + shift, Dh, 1e4)) *
+                apply_rope(y, rope_angles(pos + d + shift, Dh, 1e4)), axis=-1)
+    np.testing.assert_allclose(s1, s2, atol=1e-10, rtol=0)
+
+
+def test_rope_equals_complex_rotation_per_axis():
+    """Pair (2i, 2i+1) of section s times exp(1j * pos_s * theta^(-2i/d_s))."""
+    Dh, theta = 32, 10000.0
+    x = np.random.default_rng(8).standard_normal((1, 1, Dh))
+    pos = np.array([[3.0, 1.0, 2.0]])
+    got = apply_rope(x, rope_angles(pos, Dh, theta))[0, 0]
+    sizes, off, exp = (8, 12, 12), 0, []
+    for axis, d in enumerate(sizes):
+        zc = x[0, 0, off:off + d:2] + 1j * x[0, 0, off + 1:off + d:2]
+        zc = zc * np.exp(1j * pos[0, axis] * theta ** (-np.arange(0, d, 2) / d))
+        exp.extend(np.stack([zc.real, zc.imag], 1).ravel())
+        off += d
+    np.testing.assert_allclose(got, exp, atol=1e-14, rtol=0)
+
+
+# ----------------------------------------------------------------- shuffles
+
+def test_pixel_shuffles_match_torch_and_round_trip():
+    rng = np.random.default_rng(9)
+    zf = rng.standard_normal((16, 6, 10))
+    tok = pixel_unshuffle_frame(zf, 2)
+    ref = Fnn.pixel_unshuffle(torch.from_numpy(zf)[None], 2)[0]       # [64, 3, 5]
+    np.testing.assert_array_equal(tok, ref.permute(1, 2, 0).reshape(15, 64).numpy())
+    f = rng.standard_normal((15, 3 * 16))
+    pix = pixel_shuffle_frame(f, 3, 5, 4, 3)
+    ref = Fnn.pixel_shuffle(torch.from_numpy(f).reshape(3, 5, 48).permute(2, 0, 1)[None], 4)[0]
+    np.testing.assert_array_equal(pix, ref.numpy())
+    back = pixel_unshuffle_frame(pix, 4)
+    np.testing.assert_array_equal(back, f)
+
+
+# ----------------------------------------------------------------- window / cache
+
+def test_fig2_worked_example_three_frames_window_two():
+    """Fig. 2(a): z0 alone; z1 sees [z0, z1]; z2 sees [z1, z2] after evicting z0."""
+    cfg = replace(MICRO, window=2)
+    W, z = _micro_inputs(cfg, frames=3)
+    dec = StreamingOracle(cfg, W)
+    for t in range(3):
+        dec.decode(z[:, t:t + 1])
+    assert dec.visible_units == [[0], [0, 1], [1, 2]]
+    m = band_mask(np.arange(3), np.arange(3), 2)
+    assert m.tolist() == [[True, False, False], [True, True, False], [False, True, True]]
+    # three latent frames decode into 3 * r_t output frames (Sec. 3.4, reading O11)
+    assert dec.t == 3
+
+
+@pytest.mark.parametrize("window", [1, 2, 3])
+def test_streaming_equals_full_masked_pass(window):
+    cfg = replace(MODELS["tiny"], window=window, latent_h=4, latent_w=6)
+    W = make_weights(cfg, 11, std=0.1)
+    z = make_latents(cfg, 5, 12)
+    full = decode_full(cfg, W, z[0])
+    for fpc in (1, 5):
+        st = decode_stream(cfg, W, z, fpc)[0]
+        assert np.max(np.abs(st - full)) <= 1e-6
+        assert np.max(np.abs(st - full)) <= 1e-12
+
+
+def test_causality_future_frames_do_not_change_past_outputs():
+    cfg = replace(MODELS["tiny"], latent_h=4, latent_w=4)
+    W = make_weights(cfg, 13, std=0.1)
+    z = make_latents(cfg, 4, 14)
+    a = decode_stream(cfg, W, z, 1)
+    z2 = z.copy()
+    z2[:, :, 2:] = np.random.default_rng(0).standard_normal(z2[:, :, 2:].shape)
+    b = decode_stream(cfg, W, z2, 1)
+    r = cfg.r_t
+    assert np.array_equal(a[:, :, :2 * r], b[:, :, :2 * r])
+    assert not np.allclose(a[:, :, 2 * r:], b[:, :, 2 * r:])
+
+
+def test_window_at_least_video_length_is_block_causal_baseline():
+    """W_frm >= T' reduces to full block-causal attention (the ablation baseline)."""
+    cfg = replace(MICRO, window=3)
+    W, z = _micro_inputs(cfg, frames=3)
+    ref = _bf_array(cfg, W, z)
+    big = decode_full(replace(cfg, window=100), W, z)
+    np.testing.assert_allclose(big, ref, atol=1e-12, rtol=0)
+
+
+def test_window_one_decodes_each_frame_alone():
+    """W_frm = 1: every frame equals a fresh decode of that frame (RoPE is
+    relative, so decoding it at temporal position 0 changes nothing)."""
+    cfg = replace(MODELS["tiny"], window=1, latent_h=4, latent_w=4)
+    W = make_weights(cfg, 15, std=0.1)
+    z = make_latents(cfg, 3, 16)
+    st = decode_stream(cfg, W, z, 1)[0]
+    r = cfg.r_t
+    for t in range(3):
+        alone = decode_stream(cfg, W, z[:, :, t:t + 1], 1)[0]
+        np.testing.assert_allclose(st[:, r * t:r * (t + 1)], alone, atol=1e-12, rtol=0)
+
+
+def test_temporal_position_shift_invariance():
+    """Absolute and window-relative temporal positions give the same output
+    (Sec. 4.3 "Long Video Decoding" assigns window-relative positions)."""
+    cfg = replace(MODELS["tiny"], latent_h=4, latent_w=4)
+    W = make_weights(cfg, 17, std=0.1)
+    z = make_latents(cfg, 3, 18)[0]
+    a = StreamingOracle(cfg, W)
+    b = StreamingOracle(cfg, W)
+    b.t = 1000          # as if 1000 frames had been decoded and evicted already
+    oa = a.decode(z)
+    ob = b.decode(z)
+    np.testing.assert_allclose(oa, ob, atol=1e-9, rtol=0)
+
+
+# ----------------------------------------------------------------- closed forms
+
+def test_parameter_counts_match_table5_within_one_percent():
+    paper = {"S": (512, 8, 2, 12, 56.8), "B": (768, 12, 3, 16, 161.7),
+             "L": (1024, 16, 4, 20, 348.0), "XL": (1536, 24, 3, 20, 769.3)}
+    base = MODELS["xl-720p"]
+    for name, (D, N, G, depth, m) in paper.items():
+        cfg = replace(base, latent_channels=48, patch=1, dim=D, n_heads=N, n_kv_groups=G,
+                      n_backbone_blocks=depth, mlp_hidden=4 * D, head_hidden=4 * D)
+        assert abs(param_count(cfg) / 1e6 / m - 1) < 0.01, name
+
+
+def test_kv_cache_shape_and_bytes():
+    """Eq. kv_cache: K, V in R^{B x G x (W_frm L_frm) x D_h} per layer."""
+    cfg = MODELS["xl-720p"]
+    W = make_weights(replace(cfg, n_backbone_blocks=1, n_refine_blocks=0, latent_h=4,
+                             latent_w=4, compute_dtype="f32"), 0)
+    assert cfg.tokens_per_frame == 3600 and cfg.head_dim == 64
+    per_layer = 2 * cfg.n_kv_groups * cfg.window * cfg.tokens_per_frame * cfg.head_dim * 2
+    assert per_layer == 5_529_600    # bf16 K and V of one backbone layer at 720p
+    assert W["bb.0.wqkv"].shape == (1536 + 2 * 3 * 64, 1536)
+
+
+def test_bf16_rounding_matches_torch():
+    x = np.random.default_rng(19).standard_normal(10000).astype(np.float32) * 100
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
+    np.testing.assert_array_equal(round_to_bf16(x), ref)

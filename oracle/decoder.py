@@ -299,6 +299,7 @@ class StreamingOracle:
         self.cfg = cfg
         self.dtype = dtype
         self.W = {k: np.asarray(v, dtype=dtype) for k, v in weights.items()}
+        self.trace: Optional[List[np.ndarray]] = None  # set to [] to record residuals
         self.reset()
 
     def reset(self) -> None:
@@ -328,6 +329,8 @@ class StreamingOracle:
                 self.visible_units.append([e[0] for e in c])
             o = attention(q, kc, vc)
             x = _block_post_attention(cfg, W, p, x, o)
+            if self.trace is not None:
+                self.trace.append((name, i, x.copy()))
         return _norm(cfg, W, name + ".norm_f", x)
 
     def decode(self, z: np.ndarray) -> np.ndarray:
@@ -349,9 +352,13 @@ class StreamingOracle:
             P = np.concatenate([pixel_unshuffle_frame(z[:, u0 + f], cfg.patch)
                                 for f in range(uf)], axis=0)
             x = P @ self.W["embed.w"].T + self.W["embed.b"]
+            if self.trace is not None:
+                self.trace.append(("embed", -1, x.copy()))
             y = self._stack("bb", x, [t0 + f for f in range(uf)], unit)
             if cfg.head_kind == "temporal_first":
                 xr = _temporal_up(cfg, self.W, y, uf)
+                if self.trace is not None:
+                    self.trace.append(("tup", -1, xr.copy()))
                 taus = [r * (t0 + f) + j for f in range(uf) for j in range(r)]
                 y = self._stack("rf", xr, taus, unit)
             outs.append(_head_pixels(cfg, self.W, y, uf))

@@ -1,0 +1,111 @@
+// Internal interface between the host runtime and the gfx950 kernels.
+// Every launcher enqueues on `stream` and returns the hipError_t of the launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fd {
+
+enum class Act16 : int { F16 = 0, BF16 = 1 };  // 16-bit MFMA operand format
+
+// GEMM epilogues: C = A W^T + bias, then one of these.
+enum Epi : int {
+  EPI_STORE_F32 = 0,   // out_f[row, col] = c
+  EPI_RESID_ADD = 1,   // out_f[row, col] += c           (fp32 residual stream)
+  EPI_STORE_ACT = 2,   // out_a[row, col] = act(c)        (operand format of the next GEMM)
+  EPI_STORE_SILU = 3,  // out_a = SiLU(c)
+  EPI_STORE_GELU = 4,  // out_a = GELU(c), erf form
+  EPI_SWIGLU = 5,      // out_a[row, j] = SiLU(c_gate) * c_up, W rows interleaved per 32
+  EPI_TUP = 6,         // temporal upsampling reshape into the refinement stream (fp32)
+  EPI_PIXEL = 7,       // head output -> PixelShuffle store (+clamp), fp32 pixels
+  EPI_LINEAR_PIXEL = 8,// linear head output -> sub-frame + PixelShuffle store
+  EPI_COUNT = 9
+};
+
+struct EpiParams {
+  float* out_f = nullptr;   // fp32 destination
+  void* out_a = nullptr;    // 16-bit (or fp32 on the fp32 path) activation destination
+  int ld_out = 0;           // row stride of the destination in elements
+  const float* bias = nullptr;
+  // reshape / pixel-store geometry
+  int L = 0;                // tokens per frame
+  int r_t = 1;              // temporal factor
+  int dim = 0;              // D (temporal-up)
+  int grid_h = 0, grid_w = 0, s = 1, C = 3;
+  int frames_in = 0;        // latent frames in the call
+  int frames_out = 0;       // output frames in the call (frames_in * r_t)
+  int clamp = 1;
+};
+
+struct GemmArgs {
+  const void* A = nullptr;  // [M, K] row-major, lda
+  const void* W = nullptr;  // [N, K] row-major, ldw
+  int M = 0, N = 0, K = 0, lda = 0, ldw = 0;
+  Epi epi = EPI_STORE_F32;
+  EpiParams ep;
+};
+
+// 16-bit operand GEMM on MFMA (K % 64 == 0, lda/ldw % 8 == 0, 16-byte aligned).
+hipError_t gemm_mfma(Act16 t, const GemmArgs& g, hipStream_t stream);
+// fp32 GEMM (any shape) for the fp32 compute path.
+hipError_t gemm_f32(const GemmArgs& g, hipStream_t stream);
+
+// Attention over the rolling KV ring.
+struct AttnArgs {
+  const void* q = nullptr;     // [rows, N * D_h], rows = B * n_units * U
+  const void* k_ring = nullptr;// [B][G][S][U_pad][D_h]
+  const void* vt_ring = nullptr;// [B][G][S][D_h][U_pad]
+  void* o = nullptr;           // [rows, N * D_h]
+  int B = 1, N = 1, G = 1, Dh = 64;
+  int U = 0, U_pad = 0;        // tokens per causal unit, padded to 64
+  int S = 1;                   // ring slots
+  int n_units = 1;             // units in this call
+  int64_t u0 = 0;              // absolute index of the call's first unit
+  int window = 1;              // W_frm in units
+  float scale = 1.f;           // 1 / sqrt(D_h)
+};
+hipError_t attention_mfma(Act16 t, const AttnArgs& a, hipStream_t stream);
+hipError_t attention_f32(const AttnArgs& a, hipStream_t stream);
+
+// Norm of the fp32 residual stream into the next GEMM's operand format.
+// kind 0 = RMSNorm, 1 = LayerNorm. out_kind: 0 f16, 1 bf16, 2 fp32.
+hipError_t norm_rows(const float* x, int M, int D, const float* g, const float* b, int kind,
+                     float eps, void* out, int out_kind, hipStream_t stream);
+
+// Split raw qkv (fp32, bias included) into rotated queries and the KV ring
+// (KV-norm, RoPE) for rows of one call.
+struct QkvPostArgs {
+  const float* raw = nullptr;  // [rows, D + 2 G D_h]
+  void* q = nullptr;           // [rows, N D_h]
+  void* k_ring = nullptr;
+  void* vt_ring = nullptr;
+  const float* knorm_g = nullptr;  // [D_h] or null
+  const float* vnorm_g = nullptr;
+  const int* rope_axis = nullptr;  // [D_h / 2] axis of each pair (0 t, 1 h, 2 w)
+  const double* rope_freq = nullptr;// [D_h / 2] angular frequency of each pair
+  int rope = 1;
+  float eps = 1e-6f;
+  int B = 1, N = 1, G = 1, Dh = 64;
+  int rows_per_batch = 0;      // rows of one stream in this call
+  int L = 0;                   // tokens per (sub-)frame
+  int grid_w = 1;
+  int U = 0, U_pad = 0, S = 1; // unit geometry of the ring
+  int64_t u0 = 0;              // absolute index of the first unit of the call
+  int64_t tau0 = 0;            // temporal position of the call's first (sub-)frame
+  int out_kind = 0;            // 0 f16, 1 bf16, 2 fp32
+};
+hipError_t qkv_post(const QkvPostArgs& a, hipStream_t stream);
+
+// PixelUnshuffle + flatten of latent frames into embedding operands [B F L, K_pad].
+hipError_t unshuffle_latent(const void* z, int z_kind, int B, int C, int F, int H, int W, int p,
+                            int K_pad, void* u, int out_kind, hipStream_t stream);
+
+// h[m, j] = SiLU(raw[m, j]) * raw[m, H + j]  (fp32 path, un-interleaved weights)
+hipError_t swiglu_f32(const float* raw, int M, int H, float* h, hipStream_t stream);
+
+// Convert a host-prepared fp32 array on the device into 16-bit operands.
+hipError_t convert_f32_to_16(const float* src, void* dst, int64_t n, int out_kind,
+                             hipStream_t stream);
+
+}  // namespace fd

@@ -1,0 +1,954 @@
+// Host runtime behind include/flashdecoder.h: config validation, weight layout
+// and upload, ring / workspace allocation, and the per-chunk launch sequence of
+// the streaming decoder (Algorithm 1 of FlashDecoder for the frames of a call).
+#include "../../include/flashdecoder.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "fd_kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+fd_status fail(fd_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+#define FD_HIP(expr)                                                                   \
+  do {                                                                                 \
+    hipError_t e_ = (expr);                                                            \
+    if (e_ != hipSuccess)                                                              \
+      return fail(FD_ERR_DEVICE, "%s failed: %s", #expr, hipGetErrorString(e_));       \
+  } while (0)
+
+struct Derived {
+  int Dh, grid_h, grid_w, L, K_in, K_pad, qkv_w, act_bytes;
+  bool is16;
+  fd::Act16 a16;
+  int act_kind;  // 0 f16, 1 bf16, 2 fp32
+};
+
+bool pos_int(int v) { return v > 0; }
+
+fd_status validate(const fd_config* c, Derived* d) {
+  if (!c) return fail(FD_ERR_INVALID_ARGUMENT, "config is NULL");
+  if (c->struct_size != sizeof(fd_config))
+    return fail(FD_ERR_INVALID_ARGUMENT, "config struct_size %u != %zu", c->struct_size,
+                sizeof(fd_config));
+  if (c->compute_dtype < 0 || c->compute_dtype > 2)
+    return fail(FD_ERR_INVALID_ARGUMENT, "unknown compute_dtype %d", c->compute_dtype);
+  const int ints[] = {c->latent_channels, c->latent_h, c->latent_w, c->patch, c->dim,
+                      c->n_heads, c->n_kv_groups, c->mlp_hidden, c->r_t, c->s_out,
+                      c->out_channels, c->window, c->unit_frames, c->max_batch,
+                      c->max_frames_per_call};
+  for (int v : ints)
+    if (!pos_int(v)) return fail(FD_ERR_INVALID_ARGUMENT, "config sizes must be positive");
+  if (c->n_backbone_blocks < 0 || c->n_refine_blocks < 0)
+    return fail(FD_ERR_INVALID_ARGUMENT, "negative block count");
+  if (c->latent_h % c->patch || c->latent_w % c->patch)
+    return fail(FD_ERR_INVALID_ARGUMENT, "latent H', W' must be divisible by patch");
+  if (c->dim % c->n_heads) return fail(FD_ERR_INVALID_ARGUMENT, "dim %% n_heads != 0");
+  if (c->n_heads % c->n_kv_groups)
+    return fail(FD_ERR_INVALID_ARGUMENT, "n_heads %% n_kv_groups != 0");
+  if (c->mlp_kind != FD_MLP_SWIGLU && c->mlp_kind != FD_MLP_GELU)
+    return fail(FD_ERR_INVALID_ARGUMENT, "unknown mlp_kind");
+  if (c->norm_kind != FD_NORM_RMS && c->norm_kind != FD_NORM_LAYER)
+    return fail(FD_ERR_INVALID_ARGUMENT, "unknown norm_kind");
+  if (c->head_kind != FD_HEAD_TEMPORAL_FIRST && c->head_kind != FD_HEAD_LINEAR)
+    return fail(FD_ERR_INVALID_ARGUMENT, "unknown head_kind");
+  if (c->head_kind == FD_HEAD_TEMPORAL_FIRST && c->head_hidden <= 0)
+    return fail(FD_ERR_INVALID_ARGUMENT, "head_hidden must be positive for the temporal-first head");
+  if (!(c->norm_eps > 0.f) || !(c->rope_theta > 1.f))
+    return fail(FD_ERR_INVALID_ARGUMENT, "norm_eps must be > 0 and rope_theta > 1");
+  if (c->max_frames_per_call % c->unit_frames)
+    return fail(FD_ERR_INVALID_ARGUMENT, "max_frames_per_call must be a multiple of unit_frames");
+  Derived x{};
+  x.Dh = c->dim / c->n_heads;
+  x.grid_h = c->latent_h / c->patch;
+  x.grid_w = c->latent_w / c->patch;
+  x.L = x.grid_h * x.grid_w;
+  x.K_in = c->latent_channels * c->patch * c->patch;
+  x.is16 = c->compute_dtype != FD_DTYPE_F32;
+  x.a16 = c->compute_dtype == FD_DTYPE_BF16 ? fd::Act16::BF16 : fd::Act16::F16;
+  x.act_kind = c->compute_dtype == FD_DTYPE_F32 ? 2 : (c->compute_dtype == FD_DTYPE_BF16 ? 1 : 0);
+  x.act_bytes = x.is16 ? 2 : 4;
+  x.K_pad = x.is16 ? (x.K_in + 63) / 64 * 64 : x.K_in;
+  x.qkv_w = c->dim + 2 * c->n_kv_groups * x.Dh;
+  if (c->rope && (x.Dh % 16))
+    return fail(FD_ERR_INVALID_ARGUMENT, "3D-RoPE needs D_h %% 16 == 0 (got %d)", x.Dh);
+  if (x.Dh % 2 || x.Dh > 64)
+    return fail(FD_ERR_UNSUPPORTED, "head dim %d not supported (even, <= 64)", x.Dh);
+  if (c->dim % 4 || c->dim > 2048)
+    return fail(FD_ERR_UNSUPPORTED, "dim must be a multiple of 4 and <= 2048");
+  if (x.is16) {
+    if (x.Dh != 64) return fail(FD_ERR_UNSUPPORTED, "16-bit compute needs D_h == 64");
+    if (c->dim % 64 || c->mlp_hidden % 64 ||
+        (c->head_kind == FD_HEAD_TEMPORAL_FIRST && c->head_hidden % 64))
+      return fail(FD_ERR_UNSUPPORTED, "16-bit compute needs D, MLP and head widths %% 64 == 0");
+  } else if (x.Dh != 16 && x.Dh != 32 && x.Dh != 64) {
+    return fail(FD_ERR_UNSUPPORTED, "fp32 compute needs D_h in {16, 32, 64}");
+  }
+  if (d) *d = x;
+  return FD_OK;
+}
+
+struct TensorSpec {
+  std::string name;
+  int ndim;
+  int64_t s0, s1;
+};
+
+std::vector<TensorSpec> layout(const fd_config* c) {
+  const int D = c->dim, H = c->mlp_hidden, Dh = D / c->n_heads, G = c->n_kv_groups;
+  const bool ln = c->norm_kind == FD_NORM_LAYER;
+  const bool tf = c->head_kind == FD_HEAD_TEMPORAL_FIRST;
+  const int cs2 = c->out_channels * c->s_out * c->s_out;
+  std::vector<TensorSpec> v;
+  auto add1 = [&](const std::string& n, int64_t a) { v.push_back({n, 1, a, 0}); };
+  auto add2 = [&](const std::string& n, int64_t a, int64_t b) { v.push_back({n, 2, a, b}); };
+  auto norm = [&](const std::string& p) {
+    add1(p + ".g", D);
+    if (ln) add1(p + ".b", D);
+  };
+  add2("embed.w", D, c->latent_channels * c->patch * c->patch);
+  add1("embed.b", D);
+  const char* stacks[2] = {"bb", "rf"};
+  const int nblk[2] = {c->n_backbone_blocks, c->n_refine_blocks};
+  for (int s = 0; s < (tf ? 2 : 1); ++s) {
+    for (int i = 0; i < nblk[s]; ++i) {
+      const std::string p = std::string(stacks[s]) + "." + std::to_string(i);
+      norm(p + ".norm1");
+      add2(p + ".wqkv", D + 2 * G * Dh, D);
+      add1(p + ".bqkv", D + 2 * G * Dh);
+      if (c->kv_norm) {
+        add1(p + ".knorm.g", Dh);
+        add1(p + ".vnorm.g", Dh);
+      }
+      add2(p + ".wo", D, D);
+      add1(p + ".bo", D);
+      norm(p + ".norm2");
+      if (c->mlp_kind == FD_MLP_SWIGLU) {
+        add2(p + ".w13", 2 * H, D);
+        add1(p + ".b13", 2 * H);
+      } else {
+        add2(p + ".w1", H, D);
+        add1(p + ".b1", H);
+      }
+      add2(p + ".w2", D, H);
+      add1(p + ".b2", D);
+    }
+    norm(std::string(stacks[s]) + ".norm_f");
+    if (s == 0 && tf) {
+      add2("tup.w", (int64_t)c->r_t * D, D);
+      add1("tup.b", (int64_t)c->r_t * D);
+    }
+  }
+  if (tf) {
+    add2("head1.w", c->head_hidden, D);
+    add1("head1.b", c->head_hidden);
+    add2("head2.w", cs2, c->head_hidden);
+    add1("head2.b", cs2);
+  } else {
+    add2("head.w", (int64_t)c->r_t * cs2, D);
+    add1("head.b", (int64_t)c->r_t * cs2);
+  }
+  return v;
+}
+
+float half_bits_to_float(uint16_t h) {
+  const uint32_t s = (h >> 15) & 1, e = (h >> 10) & 31, m = h & 1023;
+  float v;
+  if (e == 0) v = std::ldexp((float)m, -24);
+  else if (e == 31) v = m ? NAN : INFINITY;
+  else v = std::ldexp((float)(m | 1024), (int)e - 25);
+  return s ? -v : v;
+}
+
+float bf16_bits_to_float(uint16_t h) {
+  uint32_t u = (uint32_t)h << 16;
+  float f;
+  std::memcpy(&f, &u, 4);
+  return f;
+}
+
+struct LayerW {
+  const void *wqkv = nullptr, *wo = nullptr, *w1 = nullptr, *w2 = nullptr;
+  const float *n1g = nullptr, *n1b = nullptr, *bqkv = nullptr, *kg = nullptr, *vg = nullptr,
+              *bo = nullptr, *n2g = nullptr, *n2b = nullptr, *b1 = nullptr, *b2 = nullptr;
+};
+
+}  // namespace
+
+struct fd_decoder {
+  fd_config cfg{};
+  Derived d{};
+  int device = 0;
+  void* wmem = nullptr;     // compute-type matrices
+  float* fmem = nullptr;    // fp32 vectors (biases, gains) and rope tables
+  void* tables = nullptr;   // rope axis / frequency tables
+  std::vector<LayerW> bb, rf;
+  const void *embed_w = nullptr, *tup_w = nullptr, *head1_w = nullptr, *head2_w = nullptr,
+             *head_w = nullptr;
+  const float *embed_b = nullptr, *bbf_g = nullptr, *bbf_b = nullptr, *rff_g = nullptr,
+              *rff_b = nullptr, *tup_b = nullptr, *head1_b = nullptr, *head2_b = nullptr,
+              *head_b = nullptr;
+  const int* rope_axis = nullptr;
+  const double* rope_freq = nullptr;
+  int live_caches = 0;
+};
+
+struct Probe {
+  int cls = -1;
+  struct Rec {
+    hipEvent_t a, b;
+    double work;
+  };
+  std::vector<Rec> pending;
+  std::vector<hipEvent_t> pool;
+  double total_ms = 0.0, work = 0.0;
+  int64_t launches = 0;
+};
+
+struct fd_kv_cache {
+  const fd_decoder* dec = nullptr;
+  int batch = 1;
+  int64_t t = 0;
+  int S = 1;
+  int U_bb = 0, U_bb_pad = 0, U_rf = 0, U_rf_pad = 0;
+  void* ring = nullptr;
+  std::vector<void*> k_bb, v_bb, k_rf, v_rf;
+  void* ws = nullptr;
+  float *x_bb = nullptr, *x_rf = nullptr, *raw = nullptr;
+  void *a = nullptr, *q = nullptr, *o = nullptr, *h = nullptr, *u = nullptr;
+  Probe probe;
+};
+
+namespace {
+
+// ---------------------------------------------------------------- probe
+
+fd_status probe_begin(fd_kv_cache* c, int cls, hipStream_t s, hipEvent_t* ev) {
+  *ev = nullptr;
+  if (c->probe.cls != cls) return FD_OK;
+  if (c->probe.pool.size() < 2) {
+    for (int i = 0; i < 64; ++i) {
+      hipEvent_t e;
+      FD_HIP(hipEventCreate(&e));
+      c->probe.pool.push_back(e);
+    }
+  }
+  *ev = c->probe.pool.back();
+  c->probe.pool.pop_back();
+  FD_HIP(hipEventRecord(*ev, s));
+  return FD_OK;
+}
+
+fd_status probe_end(fd_kv_cache* c, hipStream_t s, hipEvent_t start, double work) {
+  if (!start) return FD_OK;
+  hipEvent_t e = c->probe.pool.back();
+  c->probe.pool.pop_back();
+  FD_HIP(hipEventRecord(e, s));
+  c->probe.pending.push_back({start, e, work});
+  return FD_OK;
+}
+
+// ---------------------------------------------------------------- forward
+
+struct Ctx {
+  const fd_decoder* dec;
+  fd_kv_cache* c;
+  hipStream_t s;
+  float* trace;
+  int64_t trace_off;
+};
+
+fd_status run_gemm(Ctx& x, const fd::GemmArgs& g, double algo_k) {
+  hipEvent_t ev;
+  fd_status st = probe_begin(x.c, FD_KC_GEMM, x.s, &ev);
+  if (st) return st;
+  hipError_t e = x.dec->d.is16 ? fd::gemm_mfma(x.dec->d.a16, g, x.s) : fd::gemm_f32(g, x.s);
+  if (e != hipSuccess)
+    return fail(FD_ERR_DEVICE, "gemm launch (M=%d N=%d K=%d epi=%d) failed: %s", g.M, g.N, g.K,
+                (int)g.epi, hipGetErrorString(e));
+  return probe_end(x.c, x.s, ev, 2.0 * g.M * (double)g.N * algo_k);
+}
+
+fd::GemmArgs gemm_args(const void* A, int lda, const void* W, int M, int N, int K, fd::Epi epi,
+                       const float* bias) {
+  fd::GemmArgs g;
+  g.A = A;
+  g.W = W;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.lda = lda;
+  g.ldw = K;
+  g.epi = epi;
+  g.ep.bias = bias;
+  return g;
+}
+
+fd_status run_norm(Ctx& x, const float* src, int M, const float* g, const float* b) {
+  const fd_decoder* dec = x.dec;
+  hipEvent_t ev;
+  fd_status st = probe_begin(x.c, FD_KC_NORM, x.s, &ev);
+  if (st) return st;
+  hipError_t e = fd::norm_rows(src, M, dec->cfg.dim, g, b, dec->cfg.norm_kind, dec->cfg.norm_eps,
+                               x.c->a, dec->d.act_kind, x.s);
+  if (e != hipSuccess) return fail(FD_ERR_DEVICE, "norm launch failed: %s", hipGetErrorString(e));
+  return probe_end(x.c, x.s, ev, (double)M * dec->cfg.dim * (4.0 + dec->d.act_bytes));
+}
+
+fd_status trace_copy(Ctx& x, const float* src, int64_t n) {
+  if (!x.trace) return FD_OK;
+  FD_HIP(hipMemcpyAsync(x.trace + x.trace_off, src, n * sizeof(float), hipMemcpyDeviceToDevice, x.s));
+  x.trace_off += n;
+  return FD_OK;
+}
+
+// One transformer stack (backbone or refinement) over the rows of this call.
+fd_status run_stack(Ctx& x, const std::vector<LayerW>& layers, float* xs, int rows_per_batch,
+                    int U, int U_pad, int64_t tau0, const std::vector<void*>& kr,
+                    const std::vector<void*>& vr) {
+  const fd_decoder* dec = x.dec;
+  const fd_config& c = dec->cfg;
+  const Derived& d = dec->d;
+  fd_kv_cache* kc = x.c;
+  const int B = kc->batch;
+  const int rows = B * rows_per_batch;
+  const int D = c.dim, H = c.mlp_hidden;
+  const int n_units = rows_per_batch / U;
+  const int64_t u0 = kc->t / c.unit_frames;
+  for (size_t l = 0; l < layers.size(); ++l) {
+    const LayerW& w = layers[l];
+    fd_status st = run_norm(x, xs, rows, w.n1g, w.n1b);
+    if (st) return st;
+    fd::GemmArgs g = gemm_args(kc->a, D, w.wqkv, rows, d.qkv_w, D, fd::EPI_STORE_F32, w.bqkv);
+    g.ep.out_f = kc->raw;
+    g.ep.ld_out = d.qkv_w;
+    if ((st = run_gemm(x, g, D))) return st;
+
+    fd::QkvPostArgs qa;
+    qa.raw = kc->raw;
+    qa.q = kc->q;
+    qa.k_ring = kr[l];
+    qa.vt_ring = vr[l];
+    qa.knorm_g = c.kv_norm ? w.kg : nullptr;
+    qa.vnorm_g = c.kv_norm ? w.vg : nullptr;
+    qa.rope_axis = dec->rope_axis;
+    qa.rope_freq = dec->rope_freq;
+    qa.rope = c.rope;
+    qa.eps = c.norm_eps;
+    qa.B = B;
+    qa.N = c.n_heads;
+    qa.G = c.n_kv_groups;
+    qa.Dh = d.Dh;
+    qa.rows_per_batch = rows_per_batch;
+    qa.L = d.L;
+    qa.grid_w = d.grid_w;
+    qa.U = U;
+    qa.U_pad = U_pad;
+    qa.S = kc->S;
+    qa.u0 = u0;
+    qa.tau0 = tau0;
+    qa.out_kind = d.act_kind;
+    hipEvent_t ev;
+    if ((st = probe_begin(kc, FD_KC_QKV_POST, x.s, &ev))) return st;
+    hipError_t e = fd::qkv_post(qa, x.s);
+    if (e != hipSuccess) return fail(FD_ERR_DEVICE, "qkv_post launch failed: %s", hipGetErrorString(e));
+    if ((st = probe_end(kc, x.s, ev, (double)rows * d.qkv_w * (4.0 + d.act_bytes)))) return st;
+
+    fd::AttnArgs aa;
+    aa.q = kc->q;
+    aa.k_ring = kr[l];
+    aa.vt_ring = vr[l];
+    aa.o = kc->o;
+    aa.B = B;
+    aa.N = c.n_heads;
+    aa.G = c.n_kv_groups;
+    aa.Dh = d.Dh;
+    aa.U = U;
+    aa.U_pad = U_pad;
+    aa.S = kc->S;
+    aa.n_units = n_units;
+    aa.u0 = u0;
+    aa.window = c.window;
+    aa.scale = 1.0f / std::sqrt((float)d.Dh);
+    double keys = 0.0;  // visible keys summed over the call's query units
+    for (int lu = 0; lu < n_units; ++lu) {
+      const int64_t u = u0 + lu;
+      const int64_t vis = std::min<int64_t>(u + 1, c.window);
+      keys += (double)vis * U;
+    }
+    if ((st = probe_begin(kc, FD_KC_ATTENTION, x.s, &ev))) return st;
+    e = d.is16 ? fd::attention_mfma(d.a16, aa, x.s) : fd::attention_f32(aa, x.s);
+    if (e != hipSuccess) return fail(FD_ERR_DEVICE, "attention launch failed: %s", hipGetErrorString(e));
+    if ((st = probe_end(kc, x.s, ev, 4.0 * B * c.n_heads * (double)U * keys * d.Dh))) return st;
+
+    g = gemm_args(kc->o, D, w.wo, rows, D, D, fd::EPI_RESID_ADD, w.bo);
+    g.ep.out_f = xs;
+    g.ep.ld_out = D;
+    if ((st = run_gemm(x, g, D))) return st;
+
+    if ((st = run_norm(x, xs, rows, w.n2g, w.n2b))) return st;
+    if (c.mlp_kind == FD_MLP_SWIGLU) {
+      if (d.is16) {
+        g = gemm_args(kc->a, D, w.w1, rows, 2 * H, D, fd::EPI_SWIGLU, w.b1);
+        g.ep.out_a = kc->h;
+        g.ep.ld_out = H;
+        if ((st = run_gemm(x, g, D))) return st;
+      } else {
+        g = gemm_args(kc->a, D, w.w1, rows, 2 * H, D, fd::EPI_STORE_F32, w.b1);
+        g.ep.out_f = kc->raw;
+        g.ep.ld_out = 2 * H;
+        if ((st = run_gemm(x, g, D))) return st;
+        e = fd::swiglu_f32(kc->raw, rows, H, (float*)kc->h, x.s);
+        if (e != hipSuccess) return fail(FD_ERR_DEVICE, "swiglu launch failed: %s", hipGetErrorString(e));
+      }
+    } else {
+      g = gemm_args(kc->a, D, w.w1, rows, H, D, fd::EPI_STORE_GELU, w.b1);
+      g.ep.out_a = kc->h;
+      g.ep.ld_out = H;
+      if ((st = run_gemm(x, g, D))) return st;
+    }
+    g = gemm_args(kc->h, H, w.w2, rows, D, H, fd::EPI_RESID_ADD, w.b2);
+    g.ep.out_f = xs;
+    g.ep.ld_out = D;
+    if ((st = run_gemm(x, g, H))) return st;
+    if ((st = trace_copy(x, xs, (int64_t)rows * D))) return st;
+  }
+  return FD_OK;
+}
+
+fd_status decode(const fd_decoder* dec, const void* latent, int32_t latent_dtype, int32_t F,
+                 fd_kv_cache* kc, float* out, void* stream, float* trace, size_t trace_elems) {
+  if (!dec || !kc || !latent || !out) return fail(FD_ERR_INVALID_ARGUMENT, "NULL argument");
+  if (kc->dec != dec) return fail(FD_ERR_STATE, "cache was created by a different decoder");
+  const fd_config& c = dec->cfg;
+  const Derived& d = dec->d;
+  if (latent_dtype < 0 || latent_dtype > 2)
+    return fail(FD_ERR_INVALID_ARGUMENT, "unknown latent dtype %d", latent_dtype);
+  if (F <= 0 || F > c.max_frames_per_call || F % c.unit_frames)
+    return fail(FD_ERR_INVALID_ARGUMENT,
+                "n_frames %d must be in 1..%d and a multiple of unit_frames %d", F,
+                c.max_frames_per_call, c.unit_frames);
+  if (trace && trace_elems < fd_trace_elems(dec, kc->batch, F))
+    return fail(FD_ERR_INVALID_ARGUMENT, "trace buffer too small");
+  hipStream_t s = (hipStream_t)stream;
+  int prev_dev = 0;
+  FD_HIP(hipGetDevice(&prev_dev));
+  if (prev_dev != dec->device) FD_HIP(hipSetDevice(dec->device));
+  Ctx x{dec, kc, s, trace, 0};
+  const int B = kc->batch;
+  const int M = B * F * d.L;
+  const int D = c.dim;
+  fd_status st = FD_OK;
+  hipEvent_t ev;
+  do {
+    if ((st = probe_begin(kc, FD_KC_EMBED_IN, s, &ev))) break;
+    hipError_t e = fd::unshuffle_latent(latent, latent_dtype == FD_DTYPE_F32 ? 0 : (latent_dtype == FD_DTYPE_BF16 ? 1 : 2),
+                                        B, c.latent_channels, F, c.latent_h, c.latent_w, c.patch,
+                                        d.K_pad, kc->u, d.act_kind, s);
+    if (e != hipSuccess) { st = fail(FD_ERR_DEVICE, "unshuffle launch failed: %s", hipGetErrorString(e)); break; }
+    if ((st = probe_end(kc, s, ev, (double)M * d.K_in * (latent_dtype == FD_DTYPE_F32 ? 4 : 2) +
+                                       (double)M * d.K_pad * d.act_bytes))) break;
+    fd::GemmArgs g = gemm_args(kc->u, d.K_pad, dec->embed_w, M, D, d.K_pad, fd::EPI_STORE_F32, dec->embed_b);
+    g.ep.out_f = kc->x_bb;
+    g.ep.ld_out = D;
+    if ((st = run_gemm(x, g, d.K_in))) break;
+    if ((st = trace_copy(x, kc->x_bb, (int64_t)M * D))) break;
+    if ((st = run_stack(x, dec->bb, kc->x_bb, F * d.L, c.unit_frames * d.L, kc->U_bb_pad, kc->t,
+                        kc->k_bb, kc->v_bb))) break;
+    if ((st = run_norm(x, kc->x_bb, M, dec->bbf_g, dec->bbf_b))) break;
+    if (c.head_kind == FD_HEAD_TEMPORAL_FIRST) {
+      const int MR = M * c.r_t;
+      g = gemm_args(kc->a, D, dec->tup_w, M, c.r_t * D, D, fd::EPI_TUP, dec->tup_b);
+      g.ep.out_f = kc->x_rf;
+      g.ep.ld_out = D;
+      g.ep.L = d.L;
+      g.ep.r_t = c.r_t;
+      g.ep.dim = D;
+      if ((st = run_gemm(x, g, D))) break;
+      if ((st = trace_copy(x, kc->x_rf, (int64_t)MR * D))) break;
+      if ((st = run_stack(x, dec->rf, kc->x_rf, F * c.r_t * d.L, c.unit_frames * c.r_t * d.L,
+                          kc->U_rf_pad, kc->t * c.r_t, kc->k_rf, kc->v_rf))) break;
+      if ((st = run_norm(x, kc->x_rf, MR, dec->rff_g, dec->rff_b))) break;
+      g = gemm_args(kc->a, D, dec->head1_w, MR, c.head_hidden, D, fd::EPI_STORE_SILU, dec->head1_b);
+      g.ep.out_a = kc->h;
+      g.ep.ld_out = c.head_hidden;
+      if ((st = run_gemm(x, g, D))) break;
+      const int cs2 = c.out_channels * c.s_out * c.s_out;
+      g = gemm_args(kc->h, c.head_hidden, dec->head2_w, MR, cs2, c.head_hidden, fd::EPI_PIXEL,
+                    dec->head2_b);
+      g.ep.out_f = out;
+      g.ep.L = d.L;
+      g.ep.r_t = c.r_t;
+      g.ep.grid_h = d.grid_h;
+      g.ep.grid_w = d.grid_w;
+      g.ep.s = c.s_out;
+      g.ep.C = c.out_channels;
+      g.ep.frames_in = F;
+      g.ep.frames_out = F * c.r_t;
+      g.ep.clamp = c.clamp_output;
+      if ((st = run_gemm(x, g, c.head_hidden))) break;
+    } else {
+      const int cs2 = c.out_channels * c.s_out * c.s_out;
+      g = gemm_args(kc->a, D, dec->head_w, M, c.r_t * cs2, D, fd::EPI_LINEAR_PIXEL, dec->head_b);
+      g.ep.out_f = out;
+      g.ep.L = d.L;
+      g.ep.r_t = c.r_t;
+      g.ep.grid_h = d.grid_h;
+      g.ep.grid_w = d.grid_w;
+      g.ep.s = c.s_out;
+      g.ep.C = c.out_channels;
+      g.ep.frames_in = F;
+      g.ep.frames_out = F * c.r_t;
+      g.ep.clamp = c.clamp_output;
+      if ((st = run_gemm(x, g, D))) break;
+    }
+  } while (false);
+  if (prev_dev != dec->device) (void)hipSetDevice(prev_dev);
+  if (st != FD_OK) return st;
+  kc->t += F;
+  return FD_OK;
+}
+
+fd_status upload_weights(fd_decoder* dec, const void* w, int32_t wdt, size_t n_elems) {
+  const fd_config& c = dec->cfg;
+  const Derived& d = dec->d;
+  const std::vector<TensorSpec> specs = layout(&c);
+  size_t total = 0;
+  for (auto& t : specs) total += (size_t)t.s0 * (t.ndim == 2 ? t.s1 : 1);
+  if (n_elems != total)
+    return fail(FD_ERR_INVALID_ARGUMENT, "weight blob has %zu elements, layout needs %zu", n_elems, total);
+  // device sizes: matrices in the compute type (packed), vectors in fp32
+  auto mat_elems = [&](const TensorSpec& t) -> size_t {
+    if (t.name == "embed.w") return (size_t)t.s0 * d.K_pad;
+    return (size_t)t.s0 * t.s1;
+  };
+  size_t wbytes = 0, fbytes = 0;
+  for (auto& t : specs) {
+    if (t.ndim == 2) wbytes += (mat_elems(t) * d.act_bytes + 255) / 256 * 256;
+    else fbytes += ((size_t)t.s0 * 4 + 255) / 256 * 256;
+  }
+  if (hipMalloc(&dec->wmem, wbytes) != hipSuccess)
+    return fail(FD_ERR_OUT_OF_MEMORY, "weights: hipMalloc(%zu) failed", wbytes);
+  if (hipMalloc((void**)&dec->fmem, fbytes) != hipSuccess)
+    return fail(FD_ERR_OUT_OF_MEMORY, "vectors: hipMalloc(%zu) failed", fbytes);
+  size_t max_mat = 0;
+  for (auto& t : specs)
+    if (t.ndim == 2) max_mat = std::max(max_mat, mat_elems(t));
+  float* stage = nullptr;
+  if (d.is16 && hipMalloc((void**)&stage, max_mat * 4) != hipSuccess)
+    return fail(FD_ERR_OUT_OF_MEMORY, "staging: hipMalloc failed");
+
+  std::vector<float> host;
+  char* wp = (char*)dec->wmem;
+  char* fp = (char*)dec->fmem;
+  size_t src_off = 0;
+  const bool swiglu_pack = d.is16 && c.mlp_kind == FD_MLP_SWIGLU;
+  const int H = c.mlp_hidden;
+  fd_status st = FD_OK;
+  for (auto& t : specs) {
+    const size_t n = (size_t)t.s0 * (t.ndim == 2 ? t.s1 : 1);
+    std::vector<float> src(n);
+    for (size_t i = 0; i < n; ++i) {
+      const size_t k = src_off + i;
+      if (wdt == FD_DTYPE_F32) src[i] = ((const float*)w)[k];
+      else if (wdt == FD_DTYPE_BF16) src[i] = bf16_bits_to_float(((const uint16_t*)w)[k]);
+      else src[i] = half_bits_to_float(((const uint16_t*)w)[k]);
+    }
+    src_off += n;
+    const bool is_w13 = t.name.size() > 4 && t.name.compare(t.name.size() - 4, 4, ".w13") == 0;
+    const bool is_b13 = t.name.size() > 4 && t.name.compare(t.name.size() - 4, 4, ".b13") == 0;
+    // SwiGLU packing for the fused epilogue: rows interleaved per 32 (gate, up)
+    auto interleave = [&](const std::vector<float>& v, int64_t rowlen) {
+      std::vector<float> o(v.size());
+      for (int64_t q = 0; q < H / 32; ++q)
+        for (int e = 0; e < 32; ++e) {
+          std::memcpy(&o[(64 * q + e) * rowlen], &v[(32 * q + e) * rowlen], rowlen * 4);
+          std::memcpy(&o[(64 * q + 32 + e) * rowlen], &v[(H + 32 * q + e) * rowlen], rowlen * 4);
+        }
+      return o;
+    };
+    if (swiglu_pack && (is_w13 || is_b13)) src = interleave(src, is_w13 ? t.s1 : 1);
+    const void* dptr;
+    if (t.ndim == 2) {
+      size_t elems = mat_elems(t);
+      if (t.name == "embed.w" && d.K_pad != t.s1) {
+        host.assign(elems, 0.f);
+        for (int64_t r = 0; r < t.s0; ++r)
+          std::memcpy(&host[r * d.K_pad], &src[r * t.s1], t.s1 * 4);
+        src.swap(host);
+      }
+      if (d.is16) {
+        if (hipMemcpy(stage, src.data(), elems * 4, hipMemcpyHostToDevice) != hipSuccess ||
+            fd::convert_f32_to_16(stage, wp, elems, d.act_kind, nullptr) != hipSuccess ||
+            hipDeviceSynchronize() != hipSuccess) {
+          st = fail(FD_ERR_DEVICE, "weight upload of %s failed", t.name.c_str());
+          break;
+        }
+      } else if (hipMemcpy(wp, src.data(), elems * 4, hipMemcpyHostToDevice) != hipSuccess) {
+        st = fail(FD_ERR_DEVICE, "weight upload of %s failed", t.name.c_str());
+        break;
+      }
+      dptr = wp;
+      wp += (elems * d.act_bytes + 255) / 256 * 256;
+    } else {
+      if (hipMemcpy(fp, src.data(), n * 4, hipMemcpyHostToDevice) != hipSuccess) {
+        st = fail(FD_ERR_DEVICE, "vector upload of %s failed", t.name.c_str());
+        break;
+      }
+      dptr = fp;
+      fp += (n * 4 + 255) / 256 * 256;
+    }
+    // bind
+    const std::string& nm = t.name;
+    const float* f = (const float*)dptr;
+    if (nm == "embed.w") dec->embed_w = dptr;
+    else if (nm == "embed.b") dec->embed_b = f;
+    else if (nm == "bb.norm_f.g") dec->bbf_g = f;
+    else if (nm == "bb.norm_f.b") dec->bbf_b = f;
+    else if (nm == "rf.norm_f.g") dec->rff_g = f;
+    else if (nm == "rf.norm_f.b") dec->rff_b = f;
+    else if (nm == "tup.w") dec->tup_w = dptr;
+    else if (nm == "tup.b") dec->tup_b = f;
+    else if (nm == "head1.w") dec->head1_w = dptr;
+    else if (nm == "head1.b") dec->head1_b = f;
+    else if (nm == "head2.w") dec->head2_w = dptr;
+    else if (nm == "head2.b") dec->head2_b = f;
+    else if (nm == "head.w") dec->head_w = dptr;
+    else if (nm == "head.b") dec->head_b = f;
+    else {
+      const bool isbb = nm.compare(0, 3, "bb.") == 0;
+      const size_t dot = nm.find('.', 3);
+      const int li = std::stoi(nm.substr(3, dot - 3));
+      LayerW& L = isbb ? dec->bb[li] : dec->rf[li];
+      const std::string f2 = nm.substr(dot + 1);
+      if (f2 == "norm1.g") L.n1g = f;
+      else if (f2 == "norm1.b") L.n1b = f;
+      else if (f2 == "wqkv") L.wqkv = dptr;
+      else if (f2 == "bqkv") L.bqkv = f;
+      else if (f2 == "knorm.g") L.kg = f;
+      else if (f2 == "vnorm.g") L.vg = f;
+      else if (f2 == "wo") L.wo = dptr;
+      else if (f2 == "bo") L.bo = f;
+      else if (f2 == "norm2.g") L.n2g = f;
+      else if (f2 == "norm2.b") L.n2b = f;
+      else if (f2 == "w13" || f2 == "w1") L.w1 = dptr;
+      else if (f2 == "b13" || f2 == "b1") L.b1 = f;
+      else if (f2 == "w2") L.w2 = dptr;
+      else if (f2 == "b2") L.b2 = f;
+    }
+  }
+  if (stage) (void)hipFree(stage);
+  if (st) return st;
+
+  // 3D-RoPE tables: axis and angular frequency of every channel pair
+  const int Dh = d.Dh, np = Dh / 2;
+  std::vector<int> axis(np);
+  std::vector<double> freq(np);
+  const int sec[3] = {Dh / 4, (3 * Dh) / 8, Dh - Dh / 4 - (3 * Dh) / 8};
+  int pidx = 0;
+  for (int a = 0; a < 3; ++a)
+    for (int i = 0; i < sec[a] / 2; ++i, ++pidx) {
+      axis[pidx] = a;
+      freq[pidx] = std::pow((double)c.rope_theta, -2.0 * i / sec[a]);
+    }
+  if (hipMalloc(&dec->tables, np * (sizeof(int) + sizeof(double)) + 64) != hipSuccess)
+    return fail(FD_ERR_OUT_OF_MEMORY, "rope tables: hipMalloc failed");
+  double* fd_ = (double*)dec->tables;
+  int* ax = (int*)((char*)dec->tables + np * sizeof(double));
+  FD_HIP(hipMemcpy(fd_, freq.data(), np * sizeof(double), hipMemcpyHostToDevice));
+  FD_HIP(hipMemcpy(ax, axis.data(), np * sizeof(int), hipMemcpyHostToDevice));
+  dec->rope_freq = fd_;
+  dec->rope_axis = ax;
+  return FD_OK;
+}
+
+void free_decoder(fd_decoder* d) {
+  if (!d) return;
+  if (d->wmem) (void)hipFree(d->wmem);
+  if (d->fmem) (void)hipFree(d->fmem);
+  if (d->tables) (void)hipFree(d->tables);
+  delete d;
+}
+
+void free_cache(fd_kv_cache* c) {
+  if (!c) return;
+  if (c->ring) (void)hipFree(c->ring);
+  if (c->ws) (void)hipFree(c->ws);
+  for (auto& r : c->probe.pending) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  for (auto e : c->probe.pool) (void)hipEventDestroy(e);
+  delete c;
+}
+
+}  // namespace
+
+extern "C" {
+
+fd_status fd_config_validate(const fd_config* cfg) { return validate(cfg, nullptr); }
+
+fd_status fd_weights_layout(const fd_config* cfg, fd_tensor_desc* descs, size_t capacity,
+                            size_t* n_tensors, size_t* n_elements) {
+  fd_status st = validate(cfg, nullptr);
+  if (st != FD_OK && st != FD_ERR_UNSUPPORTED) return st;
+  try {
+    const std::vector<TensorSpec> v = layout(cfg);
+    uint64_t off = 0;
+    for (size_t i = 0; i < v.size(); ++i) {
+      if (descs && i < capacity) {
+        fd_tensor_desc& t = descs[i];
+        std::memset(&t, 0, sizeof t);
+        std::snprintf(t.name, sizeof t.name, "%s", v[i].name.c_str());
+        t.ndim = v[i].ndim;
+        t.shape[0] = v[i].s0;
+        t.shape[1] = v[i].ndim == 2 ? v[i].s1 : 0;
+        t.offset = off;
+      }
+      off += (uint64_t)v[i].s0 * (v[i].ndim == 2 ? v[i].s1 : 1);
+    }
+    if (n_tensors) *n_tensors = v.size();
+    if (n_elements) *n_elements = off;
+  } catch (...) {
+    return fail(FD_ERR_OUT_OF_MEMORY, "host allocation failed");
+  }
+  return FD_OK;
+}
+
+fd_status fd_decoder_create(const fd_config* cfg, const void* weights, int32_t weights_dtype,
+                            size_t n_elements, fd_decoder** out) {
+  if (!out) return fail(FD_ERR_INVALID_ARGUMENT, "out is NULL");
+  *out = nullptr;
+  Derived d;
+  fd_status st = validate(cfg, &d);
+  if (st) return st;
+  if (!weights) return fail(FD_ERR_INVALID_ARGUMENT, "weights is NULL");
+  if (weights_dtype < 0 || weights_dtype > 2)
+    return fail(FD_ERR_INVALID_ARGUMENT, "unknown weights dtype %d", weights_dtype);
+  fd_decoder* dec = nullptr;
+  try {
+    dec = new fd_decoder;
+    dec->cfg = *cfg;
+    dec->d = d;
+    dec->bb.resize(cfg->n_backbone_blocks);
+    dec->rf.resize(cfg->head_kind == FD_HEAD_TEMPORAL_FIRST ? cfg->n_refine_blocks : 0);
+    if (hipGetDevice(&dec->device) != hipSuccess) {
+      free_decoder(dec);
+      return fail(FD_ERR_DEVICE, "no HIP device");
+    }
+    st = upload_weights(dec, weights, weights_dtype, n_elements);
+  } catch (const std::bad_alloc&) {
+    st = fail(FD_ERR_OUT_OF_MEMORY, "host allocation failed");
+  } catch (...) {
+    st = fail(FD_ERR_DEVICE, "unexpected error while creating the decoder");
+  }
+  if (st) {
+    free_decoder(dec);
+    return st;
+  }
+  *out = dec;
+  return FD_OK;
+}
+
+void fd_decoder_destroy(fd_decoder* dec) { free_decoder(dec); }
+
+const fd_config* fd_decoder_config(const fd_decoder* dec) { return dec ? &dec->cfg : nullptr; }
+
+fd_status fd_kv_cache_create(const fd_decoder* dec, int32_t batch, fd_kv_cache** out) {
+  if (!out) return fail(FD_ERR_INVALID_ARGUMENT, "out is NULL");
+  *out = nullptr;
+  if (!dec) return fail(FD_ERR_INVALID_ARGUMENT, "decoder is NULL");
+  const fd_config& c = dec->cfg;
+  const Derived& d = dec->d;
+  if (batch < 1 || batch > c.max_batch)
+    return fail(FD_ERR_INVALID_ARGUMENT, "batch %d outside 1..%d", batch, c.max_batch);
+  fd_kv_cache* kc = nullptr;
+  try {
+    kc = new fd_kv_cache;
+  } catch (...) {
+    return fail(FD_ERR_OUT_OF_MEMORY, "host allocation failed");
+  }
+  kc->dec = dec;
+  kc->batch = batch;
+  kc->S = c.window - 1 + c.max_frames_per_call / c.unit_frames;
+  const bool tf = c.head_kind == FD_HEAD_TEMPORAL_FIRST;
+  kc->U_bb = c.unit_frames * d.L;
+  kc->U_bb_pad = (kc->U_bb + 63) / 64 * 64;
+  kc->U_rf = tf ? c.unit_frames * c.r_t * d.L : 0;
+  kc->U_rf_pad = (kc->U_rf + 63) / 64 * 64;
+  const int G = c.n_kv_groups, Dh = d.Dh;
+  const size_t es = d.act_bytes;
+  const size_t ring_bb = (size_t)batch * G * kc->S * kc->U_bb_pad * Dh * es;
+  const size_t ring_rf = (size_t)batch * G * kc->S * kc->U_rf_pad * Dh * es;
+  const int nb = c.n_backbone_blocks, nr = tf ? c.n_refine_blocks : 0;
+  const size_t ring_total = 2 * (nb * ring_bb + nr * ring_rf);
+  if (ring_total) {
+    if (hipMalloc(&kc->ring, ring_total) != hipSuccess) {
+      free_cache(kc);
+      return fail(FD_ERR_OUT_OF_MEMORY, "KV ring: hipMalloc(%zu) failed", ring_total);
+    }
+    if (hipMemset(kc->ring, 0, ring_total) != hipSuccess) {
+      free_cache(kc);
+      return fail(FD_ERR_DEVICE, "KV ring memset failed");
+    }
+  }
+  char* p = (char*)kc->ring;
+  for (int l = 0; l < nb; ++l) {
+    kc->k_bb.push_back(p); p += ring_bb;
+    kc->v_bb.push_back(p); p += ring_bb;
+  }
+  for (int l = 0; l < nr; ++l) {
+    kc->k_rf.push_back(p); p += ring_rf;
+    kc->v_rf.push_back(p); p += ring_rf;
+  }
+  // workspace
+  const int64_t M = (int64_t)batch * c.max_frames_per_call * d.L;
+  const int64_t MR = tf ? M * c.r_t : M;
+  const int D = c.dim;
+  const int64_t raw_cols = std::max<int64_t>(d.qkv_w, d.is16 ? 0 : 2 * c.mlp_hidden);
+  const int64_t hid = std::max<int64_t>(c.mlp_hidden, tf ? c.head_hidden : 0);
+  auto al = [](int64_t b) { return (size_t)((b + 255) / 256 * 256); };
+  const size_t sz_xbb = al(M * D * 4), sz_xrf = tf ? al(MR * D * 4) : 0;
+  const size_t sz_raw = al(MR * raw_cols * 4);
+  const size_t sz_a = al(MR * D * es), sz_q = sz_a, sz_o = sz_a;
+  const size_t sz_h = al(MR * hid * es), sz_u = al(M * d.K_pad * es);
+  const size_t ws = sz_xbb + sz_xrf + sz_raw + sz_a + sz_q + sz_o + sz_h + sz_u;
+  if (hipMalloc(&kc->ws, ws) != hipSuccess) {
+    free_cache(kc);
+    return fail(FD_ERR_OUT_OF_MEMORY, "workspace: hipMalloc(%zu) failed", ws);
+  }
+  p = (char*)kc->ws;
+  kc->x_bb = (float*)p; p += sz_xbb;
+  kc->x_rf = tf ? (float*)p : nullptr; p += sz_xrf;
+  kc->raw = (float*)p; p += sz_raw;
+  kc->a = p; p += sz_a;
+  kc->q = p; p += sz_q;
+  kc->o = p; p += sz_o;
+  kc->h = p; p += sz_h;
+  kc->u = p; p += sz_u;
+  *out = kc;
+  return FD_OK;
+}
+
+fd_status fd_kv_cache_reset(fd_kv_cache* cache) {
+  if (!cache) return fail(FD_ERR_INVALID_ARGUMENT, "cache is NULL");
+  cache->t = 0;
+  return FD_OK;
+}
+
+int64_t fd_kv_cache_position(const fd_kv_cache* cache) { return cache ? cache->t : -1; }
+
+void fd_kv_cache_destroy(fd_kv_cache* cache) { free_cache(cache); }
+
+fd_status fd_output_shape(const fd_decoder* dec, int32_t batch, int32_t n_frames, int64_t shape[5]) {
+  if (!dec || !shape) return fail(FD_ERR_INVALID_ARGUMENT, "NULL argument");
+  const fd_config& c = dec->cfg;
+  shape[0] = batch;
+  shape[1] = c.out_channels;
+  shape[2] = (int64_t)n_frames * c.r_t;
+  shape[3] = (int64_t)dec->d.grid_h * c.s_out;
+  shape[4] = (int64_t)dec->d.grid_w * c.s_out;
+  return FD_OK;
+}
+
+size_t fd_trace_elems(const fd_decoder* dec, int32_t batch, int32_t n_frames) {
+  if (!dec || batch < 1 || n_frames < 1) return 0;
+  const fd_config& c = dec->cfg;
+  const size_t rows = (size_t)batch * n_frames * dec->d.L;
+  size_t n = (1 + (size_t)c.n_backbone_blocks) * rows * c.dim;
+  if (c.head_kind == FD_HEAD_TEMPORAL_FIRST)
+    n += (1 + (size_t)c.n_refine_blocks) * rows * c.r_t * c.dim;
+  return n;
+}
+
+fd_status fd_decode_chunk(const fd_decoder* dec, const void* latent, int32_t latent_dtype,
+                          int32_t n_frames, fd_kv_cache* cache, float* out, void* stream) {
+  try {
+    return decode(dec, latent, latent_dtype, n_frames, cache, out, stream, nullptr, 0);
+  } catch (...) {
+    return fail(FD_ERR_DEVICE, "unexpected error in fd_decode_chunk");
+  }
+}
+
+fd_status fd_decode_chunk_trace(const fd_decoder* dec, const void* latent, int32_t latent_dtype,
+                                int32_t n_frames, fd_kv_cache* cache, float* out, void* stream,
+                                float* trace, size_t trace_elems) {
+  if (!trace) return fail(FD_ERR_INVALID_ARGUMENT, "trace is NULL");
+  try {
+    return decode(dec, latent, latent_dtype, n_frames, cache, out, stream, trace, trace_elems);
+  } catch (...) {
+    return fail(FD_ERR_DEVICE, "unexpected error in fd_decode_chunk_trace");
+  }
+}
+
+fd_status fd_probe_enable(fd_kv_cache* cache, int32_t kernel_class) {
+  if (!cache) return fail(FD_ERR_INVALID_ARGUMENT, "cache is NULL");
+  if (kernel_class >= FD_KC_COUNT) return fail(FD_ERR_INVALID_ARGUMENT, "unknown kernel class");
+  Probe& p = cache->probe;
+  for (auto& r : p.pending) {
+    (void)hipEventSynchronize(r.b);
+    p.pool.push_back(r.a);
+    p.pool.push_back(r.b);
+  }
+  p.pending.clear();
+  p.cls = kernel_class < 0 ? -1 : kernel_class;
+  p.total_ms = 0.0;
+  p.work = 0.0;
+  p.launches = 0;
+  return FD_OK;
+}
+
+fd_status fd_probe_read(fd_kv_cache* cache, double* total_ms, int64_t* launches, double* work) {
+  if (!cache) return fail(FD_ERR_INVALID_ARGUMENT, "cache is NULL");
+  Probe& p = cache->probe;
+  for (auto& r : p.pending) {
+    FD_HIP(hipEventSynchronize(r.b));
+    float ms = 0.f;
+    FD_HIP(hipEventElapsedTime(&ms, r.a, r.b));
+    p.total_ms += ms;
+    p.work += r.work;
+    p.launches += 1;
+    p.pool.push_back(r.a);
+    p.pool.push_back(r.b);
+  }
+  p.pending.clear();
+  if (total_ms) *total_ms = p.total_ms;
+  if (launches) *launches = p.launches;
+  if (work) *work = p.work;
+  return FD_OK;
+}
+
+const char* fd_status_string(fd_status s) {
+  switch (s) {
+    case FD_OK: return "ok";
+    case FD_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case FD_ERR_UNSUPPORTED: return "unsupported";
+    case FD_ERR_OUT_OF_MEMORY: return "out of memory";
+    case FD_ERR_DEVICE: return "device error";
+    case FD_ERR_STATE: return "invalid state";
+  }
+  return "unknown status";
+}
+
+const char* fd_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -12,8 +12,10 @@ trained weights, neither of which exists here):
   * Linear weights and biases: N(0, 0.02);
   * norm gains: 1 + N(0, 0.02); LayerNorm biases: N(0, 0.02);
   * drawn in fp64 from numpy PCG64 ``default_rng(seed)`` in canonical tensor
-    order, cast to fp32; configurations that compute in bf16 round every value
-    once to bf16 (round-to-nearest-even) and hand both sides the rounded values.
+    order, cast to fp32; configurations that compute with 16-bit operands
+    ("f16" or "bf16") round every weight and latent once to bf16
+    (round-to-nearest-even, the paper's training precision) and hand both
+    sides the rounded values.
 """
 from __future__ import annotations
 
@@ -31,7 +33,7 @@ __all__ = [
 @dataclass(frozen=True)
 class ModelConfig:
     """Decoder shape. Field names follow the paper's notation where it has one."""
-    compute_dtype: str          # "f32" or "bf16"
+    compute_dtype: str          # "f32", "f16" or "bf16" (16-bit MFMA operands)
     latent_channels: int        # C'
     latent_h: int               # H'
     latent_w: int               # W'
@@ -166,7 +168,7 @@ def make_weights(cfg: ModelConfig, seed: int, std: float = 0.02) -> Dict[str, np
         if kind == "g":
             a = a + 1.0
         a = a.astype(np.float32)
-        if cfg.compute_dtype == "bf16":
+        if cfg.compute_dtype != "f32":
             a = round_to_bf16(a)
         out[name] = a
     return out
@@ -177,7 +179,7 @@ def make_latents(cfg: ModelConfig, frames: int, seed: int, batch: int = 1) -> np
     rng = np.random.default_rng(seed)
     z = rng.standard_normal((batch, cfg.latent_channels, frames, cfg.latent_h, cfg.latent_w))
     z = z.astype(np.float32)
-    if cfg.compute_dtype == "bf16":
+    if cfg.compute_dtype != "f32":
         z = round_to_bf16(z)
     return z
 
@@ -225,7 +227,7 @@ TINY_ASIS = ModelConfig(
 # PixelUnshuffle(2): D=1536, 20 backbone + 2 refinement blocks, 24 heads,
 # 3 KV groups, MLP expansion 4, r_t=4, 16x16 output pixels per token, W_frm=2.
 XL_480P = ModelConfig(
-    compute_dtype="bf16", latent_channels=16, latent_h=60, latent_w=104, patch=2,
+    compute_dtype="f16", latent_channels=16, latent_h=60, latent_w=104, patch=2,
     dim=1536, n_heads=24, n_kv_groups=3, n_backbone_blocks=20, n_refine_blocks=2,
     mlp_hidden=6144, head_hidden=6144, s_out=16)
 XL_720P = replace(XL_480P, latent_h=90, latent_w=160)

@@ -41,7 +41,7 @@ __all__ = [
     "rms_norm", "layer_norm", "silu", "gelu", "rope_section_sizes",
     "rope_angles", "apply_rope", "attention", "pixel_unshuffle_frame",
     "pixel_shuffle_frame", "band_mask", "StreamingOracle", "decode_full",
-    "decode_stream",
+    "decode_stream", "block_forward", "token_positions",
 ]
 
 # --------------------------------------------------------------------------
@@ -231,6 +231,28 @@ def _block_post_attention(cfg, W, p: str, x: np.ndarray, o: np.ndarray) -> np.nd
     return x + _mlp(cfg, W, p, a)
 
 
+def block_forward(cfg, W, p: str, x: np.ndarray, pos: np.ndarray, unit: int,
+                  cache: List) -> np.ndarray:
+    """One transformer block at causal unit ``unit`` (Sec. 3.2 block, Sec. 3.3
+    cache): project, append this unit's keys / values to ``cache`` (a list of
+    (unit, k, v), oldest first), evict beyond W_frm units, attend to the whole
+    cache, then the output projection and MLP with their residual adds."""
+    a = _norm(cfg, W, p + ".norm1", x)
+    q, k, v = _qkv(cfg, W, p, a, pos)
+    cache.append((unit, k, v))
+    while len(cache) > cfg.window:           # evict the oldest unit
+        cache.pop(0)
+    kc = np.concatenate([e[1] for e in cache], axis=0)
+    vc = np.concatenate([e[2] for e in cache], axis=0)
+    o = attention(q, kc, vc)
+    return _block_post_attention(cfg, W, p, x, o)
+
+
+def token_positions(cfg, taus: Sequence[int]) -> np.ndarray:
+    """(tau, h, w) of every token of the (sub-)frames with temporal indices taus."""
+    return _positions(cfg, taus)
+
+
 def _positions(cfg, taus: Sequence[int]) -> np.ndarray:
     """(tau, h, w) of every token of the frames with temporal indices ``taus``,
     frames concatenated, tokens of a frame in raster order."""
@@ -316,19 +338,10 @@ class StreamingOracle:
         pos = _positions(cfg, taus)
         nblk = len(self.cache[name])
         for i in range(nblk):
-            p = f"{name}.{i}"
-            a = _norm(cfg, W, p + ".norm1", x)
-            q, k, v = _qkv(cfg, W, p, a, pos)
             c = self.cache[name][i]
-            c.append((unit, k, v))
-            while len(c) > cfg.window:           # evict the oldest unit
-                c.pop(0)
-            kc = np.concatenate([e[1] for e in c], axis=0)
-            vc = np.concatenate([e[2] for e in c], axis=0)
+            x = block_forward(cfg, W, f"{name}.{i}", x, pos, unit, c)
             if name == "bb" and i == 0:
                 self.visible_units.append([e[0] for e in c])
-            o = attention(q, kc, vc)
-            x = _block_post_attention(cfg, W, p, x, o)
             if self.trace is not None:
                 self.trace.append((name, i, x.copy()))
         return _norm(cfg, W, name + ".norm_f", x)

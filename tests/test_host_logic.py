@@ -1,0 +1,41 @@
+"""Host-side logic: algorithmic FLOP model and workload shapes (CPU only)."""
+from paper_2607_14898_amd.flops import call_flops
+from paper_2607_14898_amd.workloads import MODELS, WORKLOADS
+
+
+def test_attention_flops_follow_the_complexity_model():
+    """Sec. 3.3 "Complexity Analysis": attention per latent frame is
+    O(N W_frm L_frm^2 D_h); refinement works on r_t L_frm tokens with window
+    r_t W_frm L_frm. Counted as 4 N L_q L_k D_h with visible keys only."""
+    m = MODELS["xl-720p"]
+    L, N, Dh, W, r = 3600, 24, 64, 2, 4
+    _, a0 = call_flops(m, 1, 0)      # first frame: window holds itself only
+    _, a5 = call_flops(m, 1, 5)      # steady state
+    bb = lambda vis: 20 * 4 * N * L * (vis * L) * Dh
+    rf = lambda vis: 2 * 4 * N * (r * L) * (vis * r * L) * Dh
+    assert a0 == bb(1) + rf(1)
+    assert a5 == bb(W) + rf(W)
+    # a 4-frame call equals 4 one-frame calls
+    assert call_flops(m, 4, 0) == tuple(map(sum, zip(*[call_flops(m, 1, t) for t in range(4)])))
+
+
+def test_gemm_flops_of_a_steady_720p_chunk():
+    m = MODELS["xl-720p"]
+    g, a = call_flops(m, 1, 3)
+    M, D, H = 3600, 1536, 6144
+    block = 2 * M * (D * (D + 384) + D * D + 3 * D * H)
+    rblock = 2 * 4 * M * (D * (D + 384) + D * D + 3 * D * H)
+    expect = 2 * M * D * 64 + 20 * block + 2 * M * D * 4 * D + 2 * rblock + \
+        2 * 4 * M * (D * 6144 + 6144 * 768)
+    assert g == expect
+    assert abs((g + a) / 1e12 - 15.535) < 1e-3
+
+
+def test_workload_shapes():
+    wl = WORKLOADS["xl-720p-stream"]
+    m = wl.model
+    assert (m.grid_h, m.grid_w, m.tokens_per_frame) == (45, 80, 3600)
+    assert (m.out_h, m.out_w, m.pix_per_token) == (720, 1280, 768)
+    assert wl.n_calls == 32 and wl.frames_per_call == 1
+    m4 = MODELS["xl-480p"]
+    assert (m4.tokens_per_frame, m4.out_h, m4.out_w) == (1560, 480, 832)

@@ -6,13 +6,18 @@
 // slots: unit u lives in slot u mod S, K as [U_pad][D_h], V transposed as
 // [D_h][U_pad] (U_pad = U rounded up to 64, padding zero-filled once).
 //
-// 16-bit path (D_h = 64): a workgroup is 4 wave64s x 32 queries of one head.
-// Each wave computes S^T = K Q^T with the 32x32x16 MFMA so that a lane owns one
-// query and 16 key scores of each 32-key block; the online-softmax max needs a
-// single cross-half exchange per tile and the row sums stay lane-local until
-// the end. K rows are fed to the MFMA in the order that makes the score
-// registers of a lane exactly the B operand of the following P V^T MFMA, so P
-// never leaves registers. K and V^T tiles of 64 keys are double-buffered in LDS.
+// 16-bit path (D_h = 64): a workgroup is 4 wave64s; they are 4 query heads of
+// one KV group (GQA), so every K / V^T tile staged in LDS serves all four. Each
+// wave owns 64 queries as two 32-query MFMA blocks and computes S^T = K Q^T
+// with the 32x32x16 MFMA, so a lane holds one query and 16 key scores per 32-key
+// block: the softmax max needs one cross-half exchange per tile and the row
+// sums stay lane-local (v_dot2 over the f16 probabilities) until the end. K
+// rows are fed to the MFMA in the order that makes the score registers of a
+// lane exactly the B operand of the following O^T += V^T P^T MFMA, so P never
+// leaves registers. The scale folds into the exp2 argument (one FMA per
+// score), the running max is only raised when it grows by more than 2^8
+// (the accumulators are rescaled then, rarely), and only the ragged last tile
+// of a unit is masked. K and V^T tiles of 64 keys are double-buffered in LDS.
 #include "fd_kernels.h"
 
 #include <hip/hip_bf16.h>
@@ -32,6 +37,15 @@ template <> struct AMfma<_Float16> {
     return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
   }
   static __device__ __forceinline__ E cvt(float x) { return (_Float16)x; }
+  // sum of the 8 values of an operand, accumulated in fp32 (v_dot2_f32_f16)
+  static __device__ __forceinline__ float sum8(const V& p) {
+    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+    const h2 one = {(_Float16)1.f, (_Float16)1.f};
+    float acc = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; i += 2) acc = __builtin_amdgcn_fdot2((h2){p[i], p[i + 1]}, one, acc, false);
+    return acc;
+  }
 };
 template <> struct AMfma<__hip_bfloat16> {
   using V = bf16x8;
@@ -40,14 +54,22 @@ template <> struct AMfma<__hip_bfloat16> {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   }
   static __device__ __forceinline__ E cvt(float x) { return (__bf16)x; }
+  static __device__ __forceinline__ float sum8(const V& p) {
+    float acc = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc += (float)p[i];
+    return acc;
+  }
 };
 
-// LDS chunk position inside a [64 rows][8 x 16-byte chunks] tile.
-// K tiles are read by rows {0-3, 8-11} together, V^T tiles by 8 consecutive rows.
-__device__ __forceinline__ int swz_k(int row, int c) {
-  return row * 8 + (c ^ ((row & 3) | (((row >> 3) & 1) << 2)));
-}
-__device__ __forceinline__ int swz_v(int row, int c) { return row * 8 + (c ^ (row & 7)); }
+// LDS chunk position inside a [64 rows][8 x 16-byte chunks] tile. gfx950 LDS
+// serves 16 lanes of a ds_read_b128 per cycle from 16 groups of 16 bytes; chunk
+// p of row r sits in group 8 (r % 2) + p. Lanes 0-15 (and 16-31) read 16
+// distinct rows of one 16-row block -- in the order of key_of_row for K, in
+// order for V^T -- so XOR-ing the chunk with (r / 2) % 8 makes both
+// conflict-free, as well as the row-wise tile stores.
+__device__ __forceinline__ int swz_k(int row, int c) { return row * 8 + (c ^ ((row >> 1) & 7)); }
+__device__ __forceinline__ int swz_v(int row, int c) { return row * 8 + (c ^ ((row >> 1) & 7)); }
 
 // Key fed to A-operand row i of the S^T MFMA (i = 8a + 4b + c maps to key
 // 16 (a / 2) + 8 b + 4 (a % 2) + c): output register r of lane l then holds
@@ -56,150 +78,236 @@ __device__ __forceinline__ int key_of_row(int i) {
   return 16 * (i >> 4) + 8 * ((i >> 2) & 1) + 4 * ((i >> 3) & 1) + (i & 3);
 }
 
-constexpr int QT = 128;  // queries per workgroup
 constexpr int KT = 64;   // keys per tile
 
-template <typename T>
-__global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, int q_tiles) {
+// Workgroup: 4 waves = HPB heads of one KV group x (4 / HPB) query sub-tiles of
+// 64 queries. K and V^T tiles of 64 keys are shared by the 4 waves through LDS.
+template <typename T, int HPB, int NQB>
+__global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnArgs a, int q_tiles) {
   using M = AMfma<T>;
   using V = typename M::V;
+  constexpr int QW = 32 * NQB;        // queries per wave (NQB 32-query MFMA blocks)
+  constexpr int QB = QW * (4 / HPB);  // queries per workgroup
   __shared__ uint4 sk[2][KT * 8];
   __shared__ uint4 sv[2][KT * 8];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lh = lane >> 5;
-  const int n = blockIdx.y;
   const int bx = blockIdx.x;
   const int qt = bx % q_tiles, bu = bx / q_tiles;
   const int lu = bu % a.n_units, b = bu / a.n_units;
-  const int g = n / (a.N / a.G);
+  const int head0 = blockIdx.y * HPB;
+  const int n = head0 + wave % HPB;
+  const int g = head0 / (a.N / a.G);
   const int64_t u = a.u0 + lu;
   const int ldq = a.N * 64;
+  const int q0 = qt * QB + (wave / HPB) * QW;  // first query (unit-local) of this wave
 
-  // queries of this lane (clamped inside the unit; extra rows are not stored)
-  const int qi = qt * QT + wave * 32 + lr;
-  const int64_t qrow = (int64_t)(b * a.n_units + lu) * a.U + min(qi, a.U - 1);
-  const T* qp = (const T*)a.q + qrow * ldq + n * 64;
-  V qf[4];
+  // queries pre-scaled by log2(e) / sqrt(D_h): S^T then holds exp2 arguments
+  const float c = a.scale * 1.44269504088896341f;
+  V qf[NQB][4];
+  int64_t qrow[NQB];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    const uint4 v = *reinterpret_cast<const uint4*>(qp + 16 * ks + 8 * lh);
-    qf[ks] = *reinterpret_cast<const V*>(&v);
+  for (int qb = 0; qb < NQB; ++qb) {
+    const int qi = min(q0 + qb * 32 + lr, a.U - 1);
+    qrow[qb] = (int64_t)(b * a.n_units + lu) * a.U + qi;
+    const T* qp = (const T*)a.q + qrow[qb] * ldq + n * 64 + 8 * lh;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const uint4 v = *reinterpret_cast<const uint4*>(qp + 16 * ks);
+      const V raw = *reinterpret_cast<const V*>(&v);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qf[qb][ks][e] = M::cvt((float)raw[e] * c);
+    }
   }
 
   const int64_t u_lo = u - a.window + 1 > 0 ? u - a.window + 1 : 0;
-  const int n_units_vis = (int)(u - u_lo + 1);
   const int tiles_per_unit = a.U_pad / KT;
-  const int n_it = n_units_vis * tiles_per_unit;
+  const int n_it = (int)(u - u_lo + 1) * tiles_per_unit;
+  const int tail_valid = a.U - (tiles_per_unit - 1) * KT;  // keys in a unit's last tile
 
-  // global tile loads: thread handles chunks tid and tid + 256 of each tile
-  uint4 rk[2], rv[2];
-  auto gload = [&](int it) {
-    const int ku_i = it / tiles_per_unit, kt = it - ku_i * tiles_per_unit;
-    const int slot = (int)((u_lo + ku_i) % a.S);
-    const int64_t ring = ((int64_t)(b * a.G + g) * a.S + slot);
-    const T* kb = (const T*)a.k_ring + ring * a.U_pad * 64 + (int64_t)kt * KT * 64;
-    const T* vb = (const T*)a.vt_ring + ring * 64 * a.U_pad + (int64_t)kt * KT;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = tid + i * 256, r = c >> 3, cc = c & 7;
-      rk[i] = *reinterpret_cast<const uint4*>(kb + r * 64 + cc * 8);
-      rv[i] = *reinterpret_cast<const uint4*>(vb + (int64_t)r * a.U_pad + cc * 8);
+  // tile walk: (slot, tile) advanced incrementally
+  int ld_slot = (int)(u_lo % a.S), ld_kt = 0;
+  const int64_t ring0 = (int64_t)(b * a.G + g) * a.S;
+  const int c0 = tid, c1 = tid + 256;  // the two 16-byte chunks of each tile this thread moves
+  const int k_off0 = (c0 >> 3) * 64 + (c0 & 7) * 8, k_off1 = (c1 >> 3) * 64 + (c1 & 7) * 8;
+  const int v_off0 = (c0 >> 3) * a.U_pad + (c0 & 7) * 8, v_off1 = (c1 >> 3) * a.U_pad + (c1 & 7) * 8;
+  const int sk0 = swz_k(c0 >> 3, c0 & 7), sk1 = swz_k(c1 >> 3, c1 & 7);
+  const int sv0 = swz_v(c0 >> 3, c0 & 7), sv1 = swz_v(c1 >> 3, c1 & 7);
+  uint4 rk0, rk1, rv0, rv1;
+  auto gload = [&]() {
+    const int64_t ring = ring0 + ld_slot;
+    const T* kb = (const T*)a.k_ring + (ring * a.U_pad + (int64_t)ld_kt * KT) * 64;
+    const T* vb = (const T*)a.vt_ring + ring * 64 * a.U_pad + (int64_t)ld_kt * KT;
+    rk0 = *reinterpret_cast<const uint4*>(kb + k_off0);
+    rk1 = *reinterpret_cast<const uint4*>(kb + k_off1);
+    rv0 = *reinterpret_cast<const uint4*>(vb + v_off0);
+    rv1 = *reinterpret_cast<const uint4*>(vb + v_off1);
+    if (++ld_kt == tiles_per_unit) {
+      ld_kt = 0;
+      if (++ld_slot == a.S) ld_slot = 0;
     }
   };
   auto lstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = tid + i * 256, r = c >> 3, cc = c & 7;
-      sk[buf][swz_k(r, cc)] = rk[i];
-      sv[buf][swz_v(r, cc)] = rv[i];
-    }
+    sk[buf][sk0] = rk0;
+    sk[buf][sk1] = rk1;
+    sv[buf][sv0] = rv0;
+    sv[buf][sv1] = rv1;
   };
 
-  const float sl2 = a.scale * 1.44269504088896341f;  // scores in log2 units
-  float m_run = -1e30f, l_run = 0.f;
-  f32x16 acc_o[2];
+  // Running shift m_q of each query, kept as an f16 value: an extra 16-wide
+  // k-step multiplies the constant column (1, 0, ..., 0) of K with (-m_q, 0, ..)
+  // of Q, so the MFMA returns c q.k - m_q exactly and P = exp2(S^T) needs no
+  // VALU work before the exponential. The shift only has to keep P in f16
+  // range: it is raised (and O, l rescaled by the exact exp2 of the change of
+  // the f16 shifts) on the first tile and whenever some p of a lane may exceed
+  // 2^15, detected from the lane's partial row sum of the tile.
+  V kone, mqf[NQB];
 #pragma unroll
-  for (int d = 0; d < 2; ++d)
+  for (int e = 0; e < 8; ++e) {
+    kone[e] = M::cvt(e == 0 && lh == 0 ? 1.f : 0.f);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc_o[d][r] = 0.f;
-
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int it = 0; it < n_it; ++it) {
-    const int cur = it & 1;
-    if (it + 1 < n_it) gload(it + 1);
-    const int kt = it % tiles_per_unit;
-    const int valid = a.U - kt * KT;  // keys of this tile that exist
-
-    f32x16 s[2];
+    for (int qb = 0; qb < NQB; ++qb) mqf[qb][e] = M::cvt(0.f);
+  }
+  float mq[NQB], l_run[NQB];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+  for (int qb = 0; qb < NQB; ++qb) mq[qb] = l_run[qb] = 0.f;
+  f32x16 acc[NQB][2];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
-      const int krow = kb * 32 + key_of_row(lr);
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const uint4 v = sk[cur][swz_k(krow, 2 * ks + lh)];
-        s[kb] = M::run(*reinterpret_cast<const V*>(&v), qf[ks], s[kb]);
-      }
-    }
-    float mx = -1e30f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kb * 32 + 16 * (r >> 3) + 8 * lh + (r & 7);
-        const float x = key < valid ? s[kb][r] * sl2 : -INFINITY;
-        s[kb][r] = x;
-        mx = fmaxf(mx, x);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    float psum = 0.f;
-    V pf[4];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = __builtin_amdgcn_exp2f(s[kb][r] - m_new);
-        psum += p;
-        pf[kb * 2 + (r >> 3)][r & 7] = M::cvt(p);
-      }
-    l_run = l_run * alpha + psum;
+  for (int qb = 0; qb < NQB; ++qb)
 #pragma unroll
     for (int d = 0; d < 2; ++d)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc_o[d][r] *= alpha;
+      for (int r = 0; r < 16; ++r) acc[qb][d][r] = 0.f;
+
+  gload();
+  lstore(0);
+  __syncthreads();
+  int kt = 0;
+  for (int it = 0; it < n_it; ++it) {
+    const int cur = it & 1;
+    if (it + 1 < n_it) gload();
+
+    // S^T = K Q^T - m_q: lane holds query lr of each 32-query block, 16 keys per key block
+    const bool tail = kt == tiles_per_unit - 1 && tail_valid < KT;
+    if (++kt == tiles_per_unit) kt = 0;
+    f32x16 s[2][NQB];
+    auto scores = [&]() {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int qb = 0; qb < NQB; ++qb) s[kb][qb] = M::run(kone, mqf[qb], f32x16{});
+        const int krow = kb * 32 + key_of_row(lr);
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+          const uint4 v = sk[cur][swz_k(krow, 2 * ks + lh)];
+          const V kf = *reinterpret_cast<const V*>(&v);
+#pragma unroll
+          for (int qb = 0; qb < NQB; ++qb) s[kb][qb] = M::run(kf, qf[qb][ks], s[kb][qb]);
+        }
+      }
+      if (tail) {  // ragged end of a unit
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = kb * 32 + 16 * (r >> 3) + 8 * lh + (r & 7);
+            if (key >= tail_valid) {
+#pragma unroll
+              for (int qb = 0; qb < NQB; ++qb) s[kb][qb][r] = -INFINITY;
+            }
+          }
+      }
+    };
+    // P = exp2(S^T) in f16, laid out as the B operand of O^T += V^T P^T
+    V pf[NQB][4];
+    float ls[NQB];
+    auto exp_tile = [&]() {
+#pragma unroll
+      for (int qb = 0; qb < NQB; ++qb) {
+        float sum = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              pf[qb][kb * 2 + h][e] = M::cvt(__builtin_amdgcn_exp2f(s[kb][qb][8 * h + e]));
+            sum += M::sum8(pf[qb][kb * 2 + h]);
+          }
+        ls[qb] = sum;
+      }
+    };
+    scores();
+    exp_tile();
+    bool big = false;
+#pragma unroll
+    for (int qb = 0; qb < NQB; ++qb) big = big || !(ls[qb] <= 32768.f);
+    if (it == 0 || __builtin_amdgcn_ballot_w64(big) != 0) {
+      // raise the shift of every query to its tile max (never lower it); the
+      // scores are recomputed from the K tile still in LDS
+      scores();
+#pragma unroll
+      for (int qb = 0; qb < NQB; ++qb) {
+        float m0 = s[0][qb][0], m1 = s[1][qb][0];
+#pragma unroll
+        for (int r = 1; r < 16; ++r) {
+          m0 = fmaxf(m0, s[0][qb][r]);
+          m1 = fmaxf(m1, s[1][qb][r]);
+        }
+        m0 = fmaxf(m0, m1);
+        m0 = fmaxf(m0, __shfl_xor(m0, 32));
+        const float mq_new = (float)M::cvt(mq[qb] + fmaxf(m0, 0.f));
+        const float delta = mq_new - mq[qb];  // exact: both are f16 values
+        mq[qb] = mq_new;
+        mqf[qb][0] = M::cvt(lh == 0 ? -mq_new : 0.f);
+        const float alpha = __builtin_amdgcn_exp2f(-delta);
+        l_run[qb] *= alpha;
+#pragma unroll
+        for (int d = 0; d < 2; ++d)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[qb][d][r] *= alpha;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) s[kb][qb][r] -= delta;
+      }
+      exp_tile();
+    }
+#pragma unroll
+    for (int qb = 0; qb < NQB; ++qb) l_run[qb] += ls[qb];
+
 #pragma unroll
     for (int d = 0; d < 2; ++d) {
 #pragma unroll
       for (int st = 0; st < 4; ++st) {
         const uint4 v = sv[cur][swz_v(d * 32 + lr, 2 * st + lh)];
-        acc_o[d] = M::run(*reinterpret_cast<const V*>(&v), pf[st], acc_o[d]);
+        const V vf = *reinterpret_cast<const V*>(&v);
+#pragma unroll
+        for (int qb = 0; qb < NQB; ++qb) acc[qb][d] = M::run(vf, pf[qb][st], acc[qb][d]);
       }
     }
     if (it + 1 < n_it) lstore(cur ^ 1);
     __syncthreads();
   }
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
-  const float inv = 1.f / l_tot;
-  if (qi < a.U) {
-    T* op = (T*)a.o + qrow * ldq + n * 64;
 #pragma unroll
-    for (int d = 0; d < 2; ++d)
+  for (int qb = 0; qb < NQB; ++qb) {
+    const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
+    const float inv = 1.f / l_tot;
+    if (q0 + qb * 32 + lr < a.U) {
+      T* op = (T*)a.o + qrow[qb] * ldq + n * 64;
 #pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        typedef typename M::E E;
-        E o4[4];
+      for (int d = 0; d < 2; ++d)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o4[e] = M::cvt(acc_o[d][r4 * 4 + e] * inv);
-        *reinterpret_cast<uint2*>(op + d * 32 + 8 * r4 + 4 * lh) = *reinterpret_cast<uint2*>(o4);
-      }
+        for (int r4 = 0; r4 < 4; ++r4) {
+          typedef typename M::E E;
+          E o4[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o4[e] = M::cvt(acc[qb][d][r4 * 4 + e] * inv);
+          *reinterpret_cast<uint2*>(op + d * 32 + 8 * r4 + 4 * lh) = *reinterpret_cast<uint2*>(o4);
+        }
+    }
   }
 }
 
@@ -265,15 +373,37 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a, int q_tiles) {
 
 }  // namespace
 
+// Launch shape: 4 heads of a KV group per workgroup when the group has a
+// multiple of 4 query heads (GQA), and 64 queries per wave unless that leaves
+// the 256 CUs short of work (fewer than 1.5 rounds of two workgroups per CU);
+// then 32 queries per wave, which doubles the workgroups and fits three per CU.
+template <typename TT, int HPB>
+hipError_t attn_launch(const AttnArgs& a, hipStream_t s) {
+  const int blocks64 = ((a.U + 64 * (4 / HPB) - 1) / (64 * (4 / HPB))) * a.n_units * a.B * (a.N / HPB);
+  if (blocks64 >= 768) {
+    const int q_tiles = (a.U + 64 * (4 / HPB) - 1) / (64 * (4 / HPB));
+    dim3 grid(q_tiles * a.n_units * a.B, a.N / HPB);
+    hipLaunchKernelGGL((attn_mfma_kernel<TT, HPB, 2>), grid, dim3(256), 0, s, a, q_tiles);
+  } else {
+    const int q_tiles = (a.U + 32 * (4 / HPB) - 1) / (32 * (4 / HPB));
+    dim3 grid(q_tiles * a.n_units * a.B, a.N / HPB);
+    hipLaunchKernelGGL((attn_mfma_kernel<TT, HPB, 1>), grid, dim3(256), 0, s, a, q_tiles);
+  }
+  return hipGetLastError();
+}
+
 hipError_t attention_mfma(Act16 t, const AttnArgs& a, hipStream_t s) {
   if (a.Dh != 64 || a.U <= 0 || a.U_pad % 64 || a.N % a.G) return hipErrorInvalidValue;
-  const int q_tiles = (a.U + QT - 1) / QT;
-  dim3 grid(q_tiles * a.n_units * a.B, a.N);
-  if (t == Act16::F16)
-    hipLaunchKernelGGL(attn_mfma_kernel<_Float16>, grid, dim3(256), 0, s, a, q_tiles);
-  else
-    hipLaunchKernelGGL(attn_mfma_kernel<__hip_bfloat16>, grid, dim3(256), 0, s, a, q_tiles);
-  return hipGetLastError();
+  const int hpg = a.N / a.G;  // query heads per KV group
+  const int hpb = hpg % 4 == 0 ? 4 : (hpg % 2 == 0 ? 2 : 1);
+  if (t == Act16::F16) {
+    if (hpb == 4) return attn_launch<_Float16, 4>(a, s);
+    if (hpb == 2) return attn_launch<_Float16, 2>(a, s);
+    return attn_launch<_Float16, 1>(a, s);
+  }
+  if (hpb == 4) return attn_launch<__hip_bfloat16, 4>(a, s);
+  if (hpb == 2) return attn_launch<__hip_bfloat16, 2>(a, s);
+  return attn_launch<__hip_bfloat16, 1>(a, s);
 }
 
 hipError_t attention_f32(const AttnArgs& a, hipStream_t s) {

@@ -84,6 +84,8 @@ struct QkvPostArgs {
   const float* vnorm_g = nullptr;
   const int* rope_axis = nullptr;  // [D_h / 2] axis of each pair (0 t, 1 h, 2 w)
   const double* rope_freq = nullptr;// [D_h / 2] angular frequency of each pair
+  const float2* rope_hw = nullptr;  // [max(grid_h, grid_w)][D_h / 2] (cos, sin) of spatial pairs
+  float2* rope_t = nullptr;         // [(sub-)frames of the call][D_h / 2] temporal (cos, sin), filled here
   int rope = 1;
   float eps = 1e-6f;
   int B = 1, N = 1, G = 1, Dh = 64;

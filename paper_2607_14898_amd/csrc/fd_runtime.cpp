@@ -209,7 +209,7 @@ struct fd_decoder {
               *head_b = nullptr;
   const int* rope_axis = nullptr;
   const double* rope_freq = nullptr;
-  int live_caches = 0;
+  const float2* rope_hw = nullptr;
 };
 
 struct Probe {
@@ -235,6 +235,7 @@ struct fd_kv_cache {
   void* ws = nullptr;
   float *x_bb = nullptr, *x_rf = nullptr, *raw = nullptr;
   void *a = nullptr, *q = nullptr, *o = nullptr, *h = nullptr, *u = nullptr;
+  float2* rope_t = nullptr;  // temporal RoPE (cos, sin) of the current call
   Probe probe;
 };
 
@@ -352,6 +353,8 @@ fd_status run_stack(Ctx& x, const std::vector<LayerW>& layers, float* xs, int ro
     qa.vnorm_g = c.kv_norm ? w.vg : nullptr;
     qa.rope_axis = dec->rope_axis;
     qa.rope_freq = dec->rope_freq;
+    qa.rope_hw = dec->rope_hw;
+    qa.rope_t = kc->rope_t;
     qa.rope = c.rope;
     qa.eps = c.norm_eps;
     qa.B = B;
@@ -670,12 +673,24 @@ fd_status upload_weights(fd_decoder* dec, const void* w, int32_t wdt, size_t n_e
       axis[pidx] = a;
       freq[pidx] = std::pow((double)c.rope_theta, -2.0 * i / sec[a]);
     }
-  if (hipMalloc(&dec->tables, np * (sizeof(int) + sizeof(double)) + 64) != hipSuccess)
+  // spatial (cos, sin) table: entry (p, pair) for coordinate p along the pair's axis
+  const int gmax = std::max(d.grid_h, d.grid_w);
+  std::vector<float2> hw((size_t)gmax * np);
+  for (int p = 0; p < gmax; ++p)
+    for (int i = 0; i < np; ++i) {
+      const double ang = axis[i] == 0 ? 0.0 : p * freq[i];
+      hw[(size_t)p * np + i] = make_float2((float)std::cos(ang), (float)std::sin(ang));
+    }
+  const size_t tbytes = np * sizeof(double) + 256 + np * sizeof(int) + 256 + hw.size() * sizeof(float2);
+  if (hipMalloc(&dec->tables, tbytes) != hipSuccess)
     return fail(FD_ERR_OUT_OF_MEMORY, "rope tables: hipMalloc failed");
   double* fd_ = (double*)dec->tables;
-  int* ax = (int*)((char*)dec->tables + np * sizeof(double));
+  int* ax = (int*)((char*)dec->tables + np * sizeof(double) + 256);
+  float2* hwd = (float2*)((char*)ax + np * sizeof(int) + 256);
   FD_HIP(hipMemcpy(fd_, freq.data(), np * sizeof(double), hipMemcpyHostToDevice));
   FD_HIP(hipMemcpy(ax, axis.data(), np * sizeof(int), hipMemcpyHostToDevice));
+  FD_HIP(hipMemcpy(hwd, hw.data(), hw.size() * sizeof(float2), hipMemcpyHostToDevice));
+  dec->rope_hw = hwd;
   dec->rope_freq = fd_;
   dec->rope_axis = ax;
   return FD_OK;
@@ -831,7 +846,8 @@ fd_status fd_kv_cache_create(const fd_decoder* dec, int32_t batch, fd_kv_cache**
   const size_t sz_raw = al(MR * raw_cols * 4);
   const size_t sz_a = al(MR * D * es), sz_q = sz_a, sz_o = sz_a;
   const size_t sz_h = al(MR * hid * es), sz_u = al(M * d.K_pad * es);
-  const size_t ws = sz_xbb + sz_xrf + sz_raw + sz_a + sz_q + sz_o + sz_h + sz_u;
+  const size_t sz_rt = al((int64_t)c.max_frames_per_call * c.r_t * (d.Dh / 2) * sizeof(float2));
+  const size_t ws = sz_xbb + sz_xrf + sz_raw + sz_a + sz_q + sz_o + sz_h + sz_u + sz_rt;
   if (hipMalloc(&kc->ws, ws) != hipSuccess) {
     free_cache(kc);
     return fail(FD_ERR_OUT_OF_MEMORY, "workspace: hipMalloc(%zu) failed", ws);
@@ -845,6 +861,7 @@ fd_status fd_kv_cache_create(const fd_decoder* dec, int32_t batch, fd_kv_cache**
   kc->o = p; p += sz_o;
   kc->h = p; p += sz_h;
   kc->u = p; p += sz_u;
+  kc->rope_t = (float2*)p; p += sz_rt;
   *out = kc;
   return FD_OK;
 }

@@ -21,6 +21,21 @@ __device__ __forceinline__ void store_kind(void* out, int64_t i, float v, int ki
   else ((float*)out)[i] = v;
 }
 
+// Four consecutive values as one 8-byte (16-bit kinds) or 16-byte (fp32) store.
+__device__ __forceinline__ void store4(void* out, int64_t i, float4 y, int kind) {
+  if (kind == 0) {
+    typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+    const h4 h = {(_Float16)y.x, (_Float16)y.y, (_Float16)y.z, (_Float16)y.w};
+    *reinterpret_cast<h4*>((_Float16*)out + i) = h;
+  } else if (kind == 1) {
+    __hip_bfloat16 h[4] = {__float2bfloat16(y.x), __float2bfloat16(y.y), __float2bfloat16(y.z),
+                           __float2bfloat16(y.w)};
+    *reinterpret_cast<uint2*>((__hip_bfloat16*)out + i) = *reinterpret_cast<uint2*>(h);
+  } else {
+    *reinterpret_cast<float4*>((float*)out + i) = y;
+  }
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
@@ -72,74 +87,126 @@ __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, 
   for (int i = 0; i < MAXV; ++i) {
     const int c = lane + 64 * i;
     if (c < nv) {
-      const float e[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int col = 4 * c + k;
-        float y = (e[k] - mu) * rs * g[col];
-        if (KIND == 1) y += bta[col];
-        store_kind(out, (int64_t)row * D + col, y, out_kind);
+      const float4 gv = reinterpret_cast<const float4*>(g)[c];
+      float4 y = make_float4((v[i].x - mu) * rs * gv.x, (v[i].y - mu) * rs * gv.y,
+                             (v[i].z - mu) * rs * gv.z, (v[i].w - mu) * rs * gv.w);
+      if (KIND == 1) {
+        const float4 bv = reinterpret_cast<const float4*>(bta)[c];
+        y.x += bv.x; y.y += bv.y; y.z += bv.z; y.w += bv.w;
       }
+      store4(out, (int64_t)row * D + 4 * c, y, out_kind);
     }
   }
 }
 
-// One wave per (row, head slot): head slots 0..N-1 are query heads, N..N+G-1
-// key groups, N+G..N+2G-1 value groups. Lane d handles channel d (D_h <= 64).
-__global__ __launch_bounds__(256) void qkv_post_kernel(QkvPostArgs a, int rows) {
-  const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int hs = blockIdx.y;
-  if (row >= rows) return;
-  const int Dh = a.Dh;
-  const bool act = lane < Dh;
-  const int width = a.N * Dh + 2 * a.G * Dh;
-  const float x0 = act ? a.raw[(int64_t)row * width + hs * Dh + lane] : 0.f;
-  float x = x0;
-  const bool is_q = hs < a.N, is_k = !is_q && hs < a.N + a.G, is_v = hs >= a.N + a.G;
+// cos / sin of the RoPE angle of channel pair `pair` for the row (frame-or-
+// sub-frame fs of the call, token tok): temporal pairs read the per-call table
+// (fs), spatial pairs the table indexed by the token's row h or column w.
+__device__ __forceinline__ float2 rope_cs(const QkvPostArgs& a, int pair, int fs, int tok) {
+  const int axis = a.rope_axis[pair];
+  const int np = a.Dh / 2;
+  if (axis == 0) return a.rope_t[fs * np + pair];
+  const int p = axis == 1 ? tok / a.grid_w : tok % a.grid_w;
+  return a.rope_hw[p * np + pair];
+}
 
-  if (a.knorm_g && (is_k || is_v)) {  // KV-norm: RMSNorm over D_h with a learned gain
-    const float ms = wave_sum(x * x) / Dh;
-    const float* gg = is_k ? a.knorm_g : a.vnorm_g;
-    x = act ? x * rsqrtf(ms + a.eps) * gg[lane] : 0.f;
+// Queries and keys: one thread per 4 consecutive channels of a (row, head slot),
+// slots 0..N-1 query heads and N..N+G-1 key groups, so a head vector is 16
+// consecutive lanes (D_h = 64; D_h / 4 lanes in general) and consecutive
+// threads read consecutive 16-byte chunks of the raw projection.
+__global__ __launch_bounds__(256) void qk_post_kernel(QkvPostArgs a, int rows) {
+  const int Dh = a.Dh, qpv = Dh / 4;  // threads per head vector
+  const int slots = a.N + a.G;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t per_row = (int64_t)slots * qpv;
+  const bool valid = t < (int64_t)rows * per_row;
+  const int row = valid ? (int)(t / per_row) : 0;
+  const int rem = (int)(t - (int64_t)row * per_row);
+  const int hs = rem / qpv, qd = rem - hs * qpv;
+  const int width = a.N * Dh + 2 * a.G * Dh;
+  float4 x = valid ? *reinterpret_cast<const float4*>(a.raw + (int64_t)row * width + hs * Dh + 4 * qd)
+                   : make_float4(0.f, 0.f, 0.f, 0.f);
+  const bool is_q = hs < a.N;
+  if (!is_q && a.knorm_g) {  // KV-norm: RMSNorm over D_h with a learned gain
+    float ss = x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+    for (int o = qpv / 2; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+    const float r = rsqrtf(ss / Dh + a.eps);
+    const float4 gv = reinterpret_cast<const float4*>(a.knorm_g)[qd];
+    x = make_float4(x.x * r * gv.x, x.y * r * gv.y, x.z * r * gv.z, x.w * r * gv.w);
   }
+  if (!valid) return;
   const int b = row / a.rows_per_batch, rb = row - b * a.rows_per_batch;
-  const int fs = rb / a.L, tok = rb - fs * a.L;  // (sub-)frame of the call, token
-  if (a.rope && !is_v) {
-    const int pair = lane >> 1;
-    const float partner = __shfl_xor(x, 1);
-    float ang = 0.f;
-    if (act) {
-      const int axis = a.rope_axis[pair];
-      if (axis == 0) {
-        // temporal position can be large: reduce the angle in double precision
-        const double ph = (double)(a.tau0 + fs) * a.rope_freq[pair];
-        ang = (float)(ph - 6.283185307179586 * floor(ph / 6.283185307179586));
-      } else {
-        const int pos = axis == 1 ? tok / a.grid_w : tok % a.grid_w;
-        ang = (float)((double)pos * a.rope_freq[pair]);
-      }
-    }
-    float sn, cs;
-    sincosf(ang, &sn, &cs);
-    x = (lane & 1) ? partner * sn + x * cs : x * cs - partner * sn;
+  if (a.rope) {
+    const int fs = rb / a.L, tok = rb - fs * a.L;
+    const float2 c0 = rope_cs(a, 2 * qd, fs, tok), c1 = rope_cs(a, 2 * qd + 1, fs, tok);
+    x = make_float4(x.x * c0.x - x.y * c0.y, x.x * c0.y + x.y * c0.x,
+                    x.z * c1.x - x.w * c1.y, x.z * c1.y + x.w * c1.x);
   }
-  if (!act) return;
   if (is_q) {
-    store_kind(a.q, (int64_t)row * a.N * Dh + hs * Dh + lane, x, a.out_kind);
+    store4(a.q, (int64_t)row * a.N * Dh + hs * Dh + 4 * qd, x, a.out_kind);
     return;
   }
   const int lu = rb / a.U, pos = rb - lu * a.U;
   const int slot = (int)((a.u0 + lu) % a.S);
-  if (is_k) {
-    const int gk = hs - a.N;
-    const int64_t base = (((int64_t)(b * a.G + gk) * a.S + slot) * a.U_pad + pos) * Dh;
-    store_kind(a.k_ring, base + lane, x, a.out_kind);
-  } else {
-    const int gv = hs - a.N - a.G;
-    const int64_t base = (((int64_t)(b * a.G + gv) * a.S + slot) * Dh + lane) * a.U_pad + pos;
-    store_kind(a.vt_ring, base, x, a.out_kind);
+  const int64_t base = (((int64_t)(b * a.G + hs - a.N) * a.S + slot) * a.U_pad + pos) * Dh;
+  store4(a.k_ring, base + 4 * qd, x, a.out_kind);
+}
+
+// Values: one workgroup per 64 consecutive positions of one causal unit of one
+// stream and one KV group; KV-norm, then written transposed ([D_h][U_pad] per
+// slot) through LDS as rows of 64 positions.
+constexpr int VP_ROWS = 64;
+__global__ __launch_bounds__(256) void v_post_kernel(QkvPostArgs a, int blocks_per_unit) {
+  __shared__ float vt[64][VP_ROWS + 1];  // [dim][position]
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int Dh = a.Dh;
+  const bool act = lane < Dh;
+  const int g = blockIdx.y;
+  const int blk = blockIdx.x % blocks_per_unit, bu = blockIdx.x / blocks_per_unit;
+  const int units_per_batch = a.rows_per_batch / a.U;
+  const int lu = bu % units_per_batch, b = bu / units_per_batch;
+  const int pos0 = blk * VP_ROWS;
+  const int npos = min(VP_ROWS, a.U - pos0);
+  const int width = a.N * Dh + 2 * a.G * Dh;
+  constexpr int RPW = VP_ROWS / 4;
+  const int64_t row0 = (int64_t)b * a.rows_per_batch + (int64_t)lu * a.U + pos0 + wave * RPW;
+  float x[RPW];
+#pragma unroll
+  for (int i = 0; i < RPW; ++i)
+    x[i] = (act && wave * RPW + i < npos) ? a.raw[(row0 + i) * width + (a.N + a.G + g) * Dh + lane] : 0.f;
+#pragma unroll
+  for (int i = 0; i < RPW; ++i) {
+    float y = x[i];
+    if (a.vnorm_g) {
+      const float ms = wave_sum(y * y) / Dh;
+      y = act ? y * rsqrtf(ms + a.eps) * a.vnorm_g[lane] : 0.f;
+    }
+    vt[lane][wave * RPW + i] = y;
   }
+  __syncthreads();
+  const int slot = (int)((a.u0 + lu) % a.S);
+  const int64_t vbase = ((int64_t)(b * a.G + g) * a.S + slot) * Dh * a.U_pad + pos0;
+  for (int d = wave; d < Dh; d += 4)
+    if (lane < npos) store_kind(a.vt_ring, vbase + (int64_t)d * a.U_pad + lane, vt[d][lane], a.out_kind);
+}
+
+// Temporal RoPE cos / sin of the call's (sub-)frames: entry (fs, pair) for
+// position tau0 + fs; the angle is reduced modulo 2 pi in double precision so
+// that long streams keep full accuracy.
+__global__ void rope_time_kernel(int64_t tau0, int n_fs, int np, const int* axis,
+                                 const double* freq, float2* out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_fs * np) return;
+  const int fs = i / np, pair = i - fs * np;
+  float2 r = make_float2(1.f, 0.f);
+  if (axis[pair] == 0) {
+    const double ph = (double)(tau0 + fs) * freq[pair];
+    const double red = ph - 6.283185307179586 * floor(ph * 0.15915494309189535);
+    float sn, cs;
+    sincosf((float)red, &sn, &cs);
+    r = make_float2(cs, sn);
+  }
+  out[i] = r;
 }
 
 // u[(b F + f) L + h W_t + w, c p^2 + i p + j] = z[b, c, f, p h + i, p w + j]; zero padding to K_pad.
@@ -208,9 +275,18 @@ hipError_t norm_rows(const float* x, int M, int D, const float* g, const float* 
 hipError_t qkv_post(const QkvPostArgs& a, hipStream_t s) {
   const int rows = a.B * a.rows_per_batch;
   if (rows <= 0) return hipSuccess;
-  if (a.Dh > 64 || a.Dh % 2) return hipErrorInvalidValue;
-  dim3 grid((rows + 3) / 4, a.N + 2 * a.G);
-  hipLaunchKernelGGL(qkv_post_kernel, grid, dim3(256), 0, s, a, rows);
+  if (a.Dh > 64 || a.Dh % 8 || a.rows_per_batch % a.U) return hipErrorInvalidValue;
+  if (a.rope) {
+    const int n_fs = a.rows_per_batch / a.L, np = a.Dh / 2;
+    hipLaunchKernelGGL(rope_time_kernel, dim3((n_fs * np + 255) / 256), dim3(256), 0, s, a.tau0,
+                       n_fs, np, a.rope_axis, a.rope_freq, a.rope_t);
+  }
+  const int64_t threads = (int64_t)rows * (a.N + a.G) * (a.Dh / 4);
+  hipLaunchKernelGGL(qk_post_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, a, rows);
+  const int blocks_per_unit = (a.U + VP_ROWS - 1) / VP_ROWS;
+  const int units = a.B * (a.rows_per_batch / a.U);
+  hipLaunchKernelGGL(v_post_kernel, dim3(blocks_per_unit * units, a.G), dim3(256), 0, s, a,
+                     blocks_per_unit);
   return hipGetLastError();
 }
 

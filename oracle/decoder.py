@@ -41,7 +41,8 @@ __all__ = [
     "rms_norm", "layer_norm", "silu", "gelu", "rope_section_sizes",
     "rope_angles", "apply_rope", "attention", "pixel_unshuffle_frame",
     "pixel_shuffle_frame", "band_mask", "StreamingOracle", "decode_full",
-    "decode_stream", "block_forward", "token_positions",
+    "decode_stream", "block_forward", "token_positions", "block_forward_rows",
+    "stack_final", "temporal_up_rows", "head_rows",
 ]
 
 # --------------------------------------------------------------------------
@@ -246,6 +247,40 @@ def block_forward(cfg, W, p: str, x: np.ndarray, pos: np.ndarray, unit: int,
     vc = np.concatenate([e[2] for e in cache], axis=0)
     o = attention(q, kc, vc)
     return _block_post_attention(cfg, W, p, x, o)
+
+
+def block_forward_rows(cfg, W, p: str, x_keys: np.ndarray, pos_keys: np.ndarray,
+                       x_q: np.ndarray, pos_q: np.ndarray) -> np.ndarray:
+    """One block's output for a subset of query rows (Sec. 3.2 block).
+
+    ``x_keys`` [Lk, D] are the block inputs of every row whose keys and values
+    the queries see (their positions ``pos_keys``), ``x_q`` [n, D] the inputs of
+    the query rows of interest. Same arithmetic as block_forward restricted to
+    those rows: keys / values of all visible rows, queries, attention, output
+    projection and MLP only for the requested rows.
+    """
+    _, k, v = _qkv(cfg, W, p, _norm(cfg, W, p + ".norm1", x_keys), pos_keys)
+    q, _, _ = _qkv(cfg, W, p, _norm(cfg, W, p + ".norm1", x_q), pos_q)
+    o = attention(q, k, v)
+    return _block_post_attention(cfg, W, p, x_q, o)
+
+
+def stack_final(cfg, W, name: str, x: np.ndarray) -> np.ndarray:
+    """Final norm of a stack (reading: both stacks end with one)."""
+    return _norm(cfg, W, name + ".norm_f", x)
+
+
+def temporal_up_rows(cfg, W, y: np.ndarray) -> np.ndarray:
+    """Eq. temporal_upsample for rows y [n, D]: returns [n, r_t, D] (sub-frame j
+    of token row i is channel block j)."""
+    t = y @ W["tup.w"].T + W["tup.b"]
+    return t.reshape(y.shape[0], cfg.r_t, cfg.dim)
+
+
+def head_rows(cfg, W, y: np.ndarray) -> np.ndarray:
+    """Temporal-first pixel head (Sec. 3.4 Step 3) for normalised rows y [n, D]:
+    returns [n, C s^2] before PixelShuffle and clamp."""
+    return silu(y @ W["head1.w"].T + W["head1.b"]) @ W["head2.w"].T + W["head2.b"]
 
 
 def token_positions(cfg, taus: Sequence[int]) -> np.ndarray:

@@ -230,29 +230,43 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int lr = lane & 31, lk = lane >> 5;
-  auto compute_ks = [&](int buf, int ks) {
-    {
-      V a[FM], b[FN];
+  // MFMA operand fragments of one 16-wide k-step, double-buffered so that the
+  // LDS reads of step ks + 1 are in flight while the MFMAs of step ks run.
+  V fa[2][FM], fb[2][FN];
+  auto load_frags = [&](int slot, int buf, int ks) {
 #pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const uint4 v = As(buf)[swz(wm0 + i * 32 + lr, 2 * ks + lk)];
-        a[i] = *reinterpret_cast<const V*>(&v);
-      }
+    for (int i = 0; i < FM; ++i) {
+      const uint4 v = As(buf)[swz(wm0 + i * 32 + lr, 2 * ks + lk)];
+      fa[slot][i] = *reinterpret_cast<const V*>(&v);
+    }
 #pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const uint4 v = Bs(buf)[swz(wn0 + j * 32 + lr, 2 * ks + lk)];
-        b[j] = *reinterpret_cast<const V*>(&v);
-      }
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::run(a[i], b[j], acc[i][j]);
+    for (int j = 0; j < FN; ++j) {
+      const uint4 v = Bs(buf)[swz(wn0 + j * 32 + lr, 2 * ks + lk)];
+      fb[slot][j] = *reinterpret_cast<const V*>(&v);
     }
   };
-  auto compute = [&](int buf) {
+  auto mfmas = [&](int slot) {
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) compute_ks(buf, ks);
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::run(fa[slot][i], fb[slot][j], acc[i][j]);
   };
+  // One K tile from LDS buffer `buf`; `mid` runs between k-steps 1 and 2.
+  auto compute_tile = [&](int buf, auto mid) {
+    load_frags(0, buf, 0);
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      if (ks + 1 < BK / 16) {
+        load_frags((ks + 1) & 1, buf, ks + 1);
+        // issue the next step's LDS reads ahead of this step's MFMAs
+        __builtin_amdgcn_sched_group_barrier(0x100, FM + FN, 0);
+      }
+      mfmas(ks & 1);
+      __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
+      if (ks == 1) mid();
+    }
+  };
+  auto compute = [&](int buf) { compute_tile(buf, [] {}); };
 
   const int KT = K / BK;
   if constexpr (C::PF == 2) {
@@ -284,13 +298,11 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
       const int cur = kt & 1, nxt = cur ^ 1;
       const bool more = kt + 1 < KT;
       if (more) FD_GLOAD(ra0, rb0, kt + 1);
-      compute_ks(cur, 0);
-      compute_ks(cur, 1);
-      if (more) {
-        _Pragma("unroll") for (int i = 0; i < CA; ++i) As(nxt)[lds_w + i * NT] = ra0[i];
-      }
-      compute_ks(cur, 2);
-      compute_ks(cur, 3);
+      compute_tile(cur, [&] {
+        if (more) {
+          _Pragma("unroll") for (int i = 0; i < CA; ++i) As(nxt)[lds_w + i * NT] = ra0[i];
+        }
+      });
       if (more) {
         _Pragma("unroll") for (int i = 0; i < CB; ++i) Bs(nxt)[lds_w + i * NT] = rb0[i];
       }

@@ -351,3 +351,27 @@ def test_bf16_rounding_matches_torch():
     x = np.random.default_rng(19).standard_normal(10000).astype(np.float32) * 100
     ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
     np.testing.assert_array_equal(round_to_bf16(x), ref)
+
+
+def test_row_subset_block_equals_full_block():
+    """block_forward_rows (used by the full-size GPU checks) is block_forward
+    restricted to some query rows: equal to 1e-12 on every requested row."""
+    import oracle.decoder as odm
+    cfg = replace(MODELS["tiny"], latent_h=4, latent_w=6)
+    W = {k: v.astype(np.float64) for k, v in make_weights(cfg, 31, std=0.1).items()}
+    rng = np.random.default_rng(32)
+    L = cfg.tokens_per_frame
+    x0, x1 = rng.standard_normal((L, cfg.dim)), rng.standard_normal((L, cfg.dim))
+    p0, p1 = odm.token_positions(cfg, [0]), odm.token_positions(cfg, [1])
+    cache = []
+    odm.block_forward(cfg, W, "bb.0", x0, p0, 0, cache)
+    full = odm.block_forward(cfg, W, "bb.0", x1, p1, 1, cache)
+    rows = np.array([0, 5, L - 1])
+    sub = odm.block_forward_rows(cfg, W, "bb.0", np.concatenate([x0, x1]), np.concatenate([p0, p1]),
+                                 x1[rows], p1[rows])
+    np.testing.assert_allclose(sub, full[rows], atol=1e-12, rtol=0)
+    # head / temporal-up row helpers agree with the full-frame forms
+    y = odm.stack_final(cfg, W, "bb", x1)
+    t = odm.temporal_up_rows(cfg, W, y[rows])
+    full_t = odm._temporal_up(cfg, W, y, 1).reshape(cfg.r_t, L, cfg.dim)
+    np.testing.assert_allclose(t, full_t[:, rows].transpose(1, 0, 2), atol=1e-12, rtol=0)

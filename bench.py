@@ -119,7 +119,7 @@ def main() -> int:
     K = args.steps
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(K)]
-    fdb.fd_probe_enable(cache.handle, fdb.FD_KC_ATTENTION)
+    fdb.fd_probe_enable(cache.handle, fdb.FD_KC_ATTENTION_REFINE)
     flops = 0.0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -167,7 +167,7 @@ def main() -> int:
             "paper_context": "76.1 frames/s, FlashDecoder-XL Wan2.1 720p streaming, 1x H100 (Table 2)",
         },
         "roofline": {
-            "kernel": "attn_mfma_kernel<f16> (windowed GQA attention)",
+            "kernel": "attn_mfma_kernel<f16, 4 heads, 64 queries/wave> (refinement-stack attention)",
             "bound": "mfma",
             "achieved": round(achieved, 2),
             "peak": PEAK_F16_TFLOPS,

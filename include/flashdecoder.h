@@ -170,9 +170,10 @@ fd_status fd_decode_chunk_trace(const fd_decoder* dec, const void* latent, int32
 /* Number of floats fd_decode_chunk_trace writes for this batch and n_frames. */
 size_t fd_trace_elems(const fd_decoder* dec, int32_t batch, int32_t n_frames);
 
-/* Kernel classes for the event probe. */
+/* Kernel classes for the event probe. FD_KC_ATTENTION_REFINE is the subset of
+ * FD_KC_ATTENTION launched by the temporal-refinement stack. */
 enum { FD_KC_GEMM = 0, FD_KC_ATTENTION = 1, FD_KC_NORM = 2, FD_KC_QKV_POST = 3,
-       FD_KC_EMBED_IN = 4, FD_KC_COUNT = 5 };
+       FD_KC_EMBED_IN = 4, FD_KC_ATTENTION_REFINE = 5, FD_KC_COUNT = 6 };
 
 /* Event probe for measuring one kernel class inside real decode calls: when
  * enabled on a cache, every launch of that class made by fd_decode_chunk is

@@ -243,9 +243,9 @@ namespace {
 
 // ---------------------------------------------------------------- probe
 
-fd_status probe_begin(fd_kv_cache* c, int cls, hipStream_t s, hipEvent_t* ev) {
+fd_status probe_begin(fd_kv_cache* c, int cls, hipStream_t s, hipEvent_t* ev, int cls2 = -1) {
   *ev = nullptr;
-  if (c->probe.cls != cls) return FD_OK;
+  if (c->probe.cls != cls && (cls2 < 0 || c->probe.cls != cls2)) return FD_OK;
   if (c->probe.pool.size() < 2) {
     for (int i = 0; i < 64; ++i) {
       hipEvent_t e;
@@ -325,7 +325,7 @@ fd_status trace_copy(Ctx& x, const float* src, int64_t n) {
 // One transformer stack (backbone or refinement) over the rows of this call.
 fd_status run_stack(Ctx& x, const std::vector<LayerW>& layers, float* xs, int rows_per_batch,
                     int U, int U_pad, int64_t tau0, const std::vector<void*>& kr,
-                    const std::vector<void*>& vr) {
+                    const std::vector<void*>& vr, bool refine) {
   const fd_decoder* dec = x.dec;
   const fd_config& c = dec->cfg;
   const Derived& d = dec->d;
@@ -398,7 +398,8 @@ fd_status run_stack(Ctx& x, const std::vector<LayerW>& layers, float* xs, int ro
       const int64_t vis = std::min<int64_t>(u + 1, c.window);
       keys += (double)vis * U;
     }
-    if ((st = probe_begin(kc, FD_KC_ATTENTION, x.s, &ev))) return st;
+    if ((st = probe_begin(kc, FD_KC_ATTENTION, x.s, &ev, refine ? FD_KC_ATTENTION_REFINE : -1)))
+      return st;
     e = d.is16 ? fd::attention_mfma(d.a16, aa, x.s) : fd::attention_f32(aa, x.s);
     if (e != hipSuccess) return fail(FD_ERR_DEVICE, "attention launch failed: %s", hipGetErrorString(e));
     if ((st = probe_end(kc, x.s, ev, 4.0 * B * c.n_heads * (double)U * keys * d.Dh))) return st;
@@ -476,7 +477,7 @@ fd_status decode(const fd_decoder* dec, const void* latent, int32_t latent_dtype
     if ((st = run_gemm(x, g, d.K_in))) break;
     if ((st = trace_copy(x, kc->x_bb, (int64_t)M * D))) break;
     if ((st = run_stack(x, dec->bb, kc->x_bb, F * d.L, c.unit_frames * d.L, kc->U_bb_pad, kc->t,
-                        kc->k_bb, kc->v_bb))) break;
+                        kc->k_bb, kc->v_bb, false))) break;
     if ((st = run_norm(x, kc->x_bb, M, dec->bbf_g, dec->bbf_b))) break;
     if (c.head_kind == FD_HEAD_TEMPORAL_FIRST) {
       const int MR = M * c.r_t;
@@ -489,7 +490,7 @@ fd_status decode(const fd_decoder* dec, const void* latent, int32_t latent_dtype
       if ((st = run_gemm(x, g, D))) break;
       if ((st = trace_copy(x, kc->x_rf, (int64_t)MR * D))) break;
       if ((st = run_stack(x, dec->rf, kc->x_rf, F * c.r_t * d.L, c.unit_frames * c.r_t * d.L,
-                          kc->U_rf_pad, kc->t * c.r_t, kc->k_rf, kc->v_rf))) break;
+                          kc->U_rf_pad, kc->t * c.r_t, kc->k_rf, kc->v_rf, true))) break;
       if ((st = run_norm(x, kc->x_rf, MR, dec->rff_g, dec->rff_b))) break;
       g = gemm_args(kc->a, D, dec->head1_w, MR, c.head_hidden, D, fd::EPI_STORE_SILU, dec->head1_b);
       g.ep.out_a = kc->h;

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libflashdecoder.so")
 FD_OK, FD_ERR_INVALID_ARGUMENT, FD_ERR_UNSUPPORTED, FD_ERR_OUT_OF_MEMORY, FD_ERR_DEVICE, \
     FD_ERR_STATE = range(6)
 FD_DTYPE_F32, FD_DTYPE_BF16, FD_DTYPE_F16 = 0, 1, 2
-FD_KC_GEMM, FD_KC_ATTENTION, FD_KC_NORM, FD_KC_QKV_POST, FD_KC_EMBED_IN = range(5)
+FD_KC_GEMM, FD_KC_ATTENTION, FD_KC_NORM, FD_KC_QKV_POST, FD_KC_EMBED_IN, FD_KC_ATTENTION_REFINE = range(6)
 
 _DTYPES = {"f32": FD_DTYPE_F32, "bf16": FD_DTYPE_BF16, "f16": FD_DTYPE_F16}
 

@@ -46,7 +46,7 @@ struct GemmArgs {
   EpiParams ep;
 };
 
-// 16-bit operand GEMM on MFMA (K % 64 == 0, lda/ldw % 8 == 0, 16-byte aligned).
+// 16-bit operand GEMM on MFMA (K > 0, K % 32 == 0, lda/ldw % 8 == 0, 16-byte aligned).
 hipError_t gemm_mfma(Act16 t, const GemmArgs& g, hipStream_t stream);
 // fp32 GEMM (any shape) for the fp32 compute path.
 hipError_t gemm_f32(const GemmArgs& g, hipStream_t stream);

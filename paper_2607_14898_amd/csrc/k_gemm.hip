@@ -7,11 +7,13 @@
 // projection: bias, residual add into the fp32 stream, SiLU / GELU / SwiGLU,
 // the channel -> sub-frame reshape of Step 1 and the PixelShuffle store.
 //
-// 16-bit path: one workgroup of 4 wave64s computes a BM x BN tile with the
-// gfx950 32x32x16 MFMA (fp32 accumulate). A and W are both K-contiguous, so
-// both operands are read from LDS with 16-byte ds_read_b128 per lane; tiles of
-// 64 K-columns are double-buffered in LDS with a per-row XOR swizzle of the
-// 16-byte chunks (conflict-free for the 16 rows a ds_read_b128 serves at once).
+// 16-bit path: one workgroup of wave64s computes a BM x BN tile with the
+// gfx950 32x32x16 MFMA (fp32 accumulate). A and W are both K-contiguous; K
+// tiles of 32 columns are copied from memory straight into LDS by the buffer
+// unit (buffer_load ... lds, no register staging) several tiles ahead of the
+// MFMAs, and read back as MFMA fragments with 16-byte ds_read_b128 per lane
+// through a per-row XOR swizzle of the 16-byte chunks that keeps the 16 rows
+// one ds_read_b128 serves at once in 16 different bank groups.
 #include "fd_kernels.h"
 
 #include <hip/hip_bf16.h>
@@ -125,25 +127,10 @@ template <> struct Mfma<__hip_bfloat16> {
   }
 };
 
-constexpr int BK = 64;   // K-columns per LDS tile: 8 chunks of 16 bytes per row
-
-// Physical 16-byte chunk of (row, chunk) inside a [rows][8 chunks] LDS tile.
-// gfx950 LDS serves 16 lanes of a ds_read_b128 per cycle from 64 banks, i.e.
-// 16 groups of 16 bytes; chunk p of row r sits in group 8 (r % 2) + p. XOR-ing
-// the chunk with (r / 2) % 8 puts the 16 consecutive rows a wave reads together
-// in 16 different groups (and keeps the row-wise stores conflict-free).
-__device__ __forceinline__ int swz(int row, int chunk) {
-  return row * 8 + (chunk ^ ((row >> 1) & 7));
-}
-
 // Raw buffer resource over `bytes` bytes at `base`: loads at offsets past the
 // end return zeros, which covers the ragged M / N edges of a tile.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
-}
-__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t soff) {
-  auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, soff, 0);
-  return *reinterpret_cast<uint4*>(&v);
 }
 
 // Workgroup -> output tile. The hardware deals workgroups round-robin to the 8
@@ -164,62 +151,149 @@ __device__ __forceinline__ void tile_of(int bid, int n_tiles, int tiles_m, int t
   tn = in / gm;
 }
 
-// Tile configuration of the MFMA GEMM: BM x BN output tile, WAVES_M x WAVES_N
-// wave64s (each a (BM / WAVES_M) x (BN / WAVES_N) sub-tile of 32x32 MFMA
-// blocks), PF = 1 or 2 K-tiles of global loads in flight in registers.
-template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int PF_>
+// Epilogue of one wave's FM x FN blocks of 32 x 32 accumulators whose first
+// output row / column are r0 / c0. MFMA accumulator layout: lane (lk, lr) holds
+// column lr of each block and rows 8 (r / 4) + 4 lk + r % 4 for r = 0..15.
+template <int EPI, typename T, int FM, int FN>
+__device__ __forceinline__ void store_tile(const EpiParams& ep, const f32x16 (&acc)[FM][FN], int r0,
+                                           int c0, int M, int N, int lr, int lk) {
+  if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = r0 + i * 32 + 8 * (r >> 2) + 4 * lk + (r & 3);
+        if (row >= M) continue;
+#pragma unroll
+        for (int j = 0; j < FN; j += 2) {
+          const int pc = c0 + j * 32 + lr;  // packed gate column; up is +32
+          if (pc >= N) continue;
+          const float g = acc[i][j][r] + ep.bias[pc];
+          const float u = acc[i][j + 1][r] + ep.bias[pc + 32];
+          const int oc = (c0 + j * 32) / 2 + lr;
+          ((T*)ep.out_a)[(int64_t)row * ep.ld_out + oc] = to_act<T>(silu_f(g) * u);
+        }
+      }
+  } else {
+    int64_t coff[FN];
+    float cb[FN];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int col = min(c0 + j * 32 + lr, N - 1);
+      coff[j] = col_off<EPI>(ep, col);
+      cb[j] = ep.bias[col];
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = r0 + i * 32 + 8 * (r >> 2) + 4 * lk + (r & 3);
+        if (row >= M) continue;
+        const int64_t ro = row_off<EPI>(ep, row);
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          if (c0 + j * 32 + lr < N) epi_store<EPI, T>(ep, ro + coff[j], acc[i][j][r] + cb[j]);
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 16-bit MFMA GEMM. K tiles of 32 columns go from memory straight into LDS
+// with buffer_load_dwordx4 ... lds (no register staging, no LDS store
+// instructions), NS tiles deep: while tile t is multiplied, tiles t + 1 ..
+// t + NS - 1 are in flight. A DMA instruction writes the 16 bytes of lane l to
+// LDS slot l after a wave-uniform base, so the bank swizzle is applied on the
+// global side: lane l fetches the chunk that belongs in slot l.
+// ---------------------------------------------------------------------------
+constexpr int BKD = 32;  // K-columns per stage: 4 chunks of 16 bytes per row
+
+// Tile configuration: BM x BN output tile, WAVES_M x WAVES_N wave64s (each a
+// (BM / WAVES_M) x (BN / WAVES_N) sub-tile of 32 x 32 MFMA blocks), NS stages.
+template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int NS_>
 struct TileCfg {
-  static constexpr int BM = BM_, BN = BN_, WAVES_M = WAVES_M_, WAVES_N = WAVES_N_, PF = PF_;
-  static constexpr int NT = 64 * WAVES_M * WAVES_N;
-  static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
-  static constexpr int FM = WM / 32, FN = WN / 32;
-  static constexpr int CA = BM * 8 / NT, CB = BN * 8 / NT;  // 16-byte chunks per thread
-  static constexpr int LDS_BYTES = 2 * (BM + BN) * BK * 2;
-  static constexpr int MIN_BLOCKS = (163840 / LDS_BYTES) < 2 ? 1 : 2;
+  static constexpr int BM = BM_, BN = BN_, WAVES_M = WAVES_M_, WAVES_N = WAVES_N_, NS = NS_;
+  static constexpr int NW = WAVES_M * WAVES_N, NT = 64 * NW;
+  static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N, FM = WM / 32, FN = WN / 32;
+  static constexpr int STAGE = (BM + BN) * 4;                 // 16-byte slots per stage
+  static constexpr int QA = BM / 16 / NW, QB = BN / 16 / NW;  // DMAs per thread and stage
+  static constexpr int LDS_BYTES = NS * STAGE * 16;
+  static constexpr int MIN_BLOCKS = 163840 / LDS_BYTES >= 2 ? 2 : 1;
+  static_assert(BM % (16 * NW) == 0 && BN % (16 * NW) == 0, "DMA rows split evenly over waves");
+  static_assert(NS >= 3 && LDS_BYTES <= 163840, "at least 3 stages, within 160 KB of LDS");
+  static_assert((NS - 2) * (QA + QB) < 64, "vmcnt range");
 };
 
+// s_waitcnt immediates (gfx9 encoding): vmcnt(n) with lgkmcnt and expcnt
+// untouched, and lgkmcnt(0) alone.
+#define FD_VMCNT(n) ((((n) & 0xF) | ((((n) >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8)))
+#define FD_LGKMCNT0 (0xF | (0x3 << 14) | (0x7 << 4))
+
+// Stage row r (A rows 0..BM-1, then W rows) holds K-chunk c of that row in
+// physical slot 4 r + (c ^ ((r / 4) % 4)): the 16 rows one ds_read_b128 serves
+// at once then cover all 16 bank groups.
+//
+// The DMAs are issued from inline assembly (M0 = LDS destination of the wave),
+// so the compiler neither sees nor orders them; every ordering they need is
+// explicit: s_waitcnt on the wave's own DMAs, then s_barrier (with compiler
+// memory barriers around it) before any wave reads the tile or refills a stage.
 template <typename T, class C, int EPI>
 __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
     const T* __restrict__ A, const T* __restrict__ W, int M, int N, int K, int lda, int ldw,
     EpiParams ep, int tiles_m, int tiles_n) {
-  constexpr int BM = C::BM, BN = C::BN, FM = C::FM, FN = C::FN, CA = C::CA, CB = C::CB;
-  constexpr int NT = C::NT;
+  constexpr int BM = C::BM, BN = C::BN, FM = C::FM, FN = C::FN, NS = C::NS, NW = C::NW;
+  constexpr int QA = C::QA, Q = C::QA + C::QB, STAGE = C::STAGE;
   using V = typename Mfma<T>::V;
+  __shared__ uint4 lds[NS * STAGE];
 
-  extern __shared__ uint4 lds[];
-  // LDS buffer b: A tile at lds + b (BM + BN) 8, W tile right after it
-  auto As = [&](int b) { return lds + b * (BM + BN) * 8; };
-  auto Bs = [&](int b) { return lds + b * (BM + BN) * 8 + BM * 8; };
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   int tm, tn;
   tile_of(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int wm0 = (wave / C::WAVES_N) * C::WM, wn0 = (wave % C::WAVES_N) * C::WN;
 
-  // global -> register staging through buffer loads; chunk i of this thread is
-  // row (tid / 8) + (NT / 8) i, 16-byte column (tid % 8) of the tile
   const __amdgpu_buffer_rsrc_t rA =
       make_rsrc(A + (int64_t)m0 * lda, (uint32_t)min(BM, M - m0) * lda * (uint32_t)sizeof(T));
   const __amdgpu_buffer_rsrc_t rB =
       make_rsrc(W + (int64_t)n0 * ldw, (uint32_t)min(BN, N - n0) * ldw * (uint32_t)sizeof(T));
-  const uint32_t offA = ((tid >> 3) * lda + (tid & 7) * 8) * (uint32_t)sizeof(T);
-  const uint32_t offB = ((tid >> 3) * ldw + (tid & 7) * 8) * (uint32_t)sizeof(T);
-  constexpr int RSTEP = NT / 8;  // rows between a thread's chunks
-  const uint32_t stepA = RSTEP * lda * (uint32_t)sizeof(T), stepB = RSTEP * ldw * (uint32_t)sizeof(T);
-  const int lds_w = swz(tid >> 3, tid & 7);  // + NT i for chunk i
-  uint4 ra0[CA], rb0[CB], ra1[C::PF == 2 ? CA : 1], rb1[C::PF == 2 ? CB : 1];
-#define FD_GLOAD(RA, RB, KT)                                                   \
-  do {                                                                         \
-    const uint32_t koff = (KT) * BK * (uint32_t)sizeof(T);                     \
-    _Pragma("unroll") for (int i = 0; i < CA; ++i) RA[i] = buf_load16(rA, offA + i * stepA, koff); \
-    _Pragma("unroll") for (int i = 0; i < CB; ++i) RB[i] = buf_load16(rB, offB + i * stepB, koff); \
-  } while (0)
-#define FD_LSTORE(RA, RB, BUF)                                                 \
-  do {                                                                         \
-    _Pragma("unroll") for (int i = 0; i < CA; ++i) As(BUF)[lds_w + i * NT] = RA[i]; \
-    _Pragma("unroll") for (int i = 0; i < CB; ++i) Bs(BUF)[lds_w + i * NT] = RB[i]; \
-  } while (0)
+  // DMA j of this wave fills stage rows 16 q .. 16 q + 15, q = j NW + wave (A
+  // rows for j < QA, W rows after); lane l lands in row 16 q + l / 4, physical
+  // chunk l % 4, which holds K-chunk (l % 4) ^ ((l / 16) % 4).
+  const int lrow = lane >> 2, lchunk = (lane & 3) ^ ((lane >> 4) & 3);
+  uint32_t voff[Q];
+#pragma unroll
+  for (int j = 0; j < Q; ++j) {
+    const int row = 16 * (j * NW + wave) + lrow - (j < QA ? 0 : BM);
+    voff[j] = (uint32_t)(row * (j < QA ? lda : ldw) + lchunk * 8) * (uint32_t)sizeof(T);
+  }
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint4*)lds;
+  auto dma = [&](int st, int kt) {
+    const uint32_t soff = (uint32_t)kt * BKD * (uint32_t)sizeof(T);
+#pragma unroll
+    for (int j = 0; j < Q; ++j) {
+      const uint32_t m0addr = lds0 + (uint32_t)(st * STAGE + 64 * (j * NW + wave)) * 16u;
+      // M0 is reserved by the compiler, but nothing else in this kernel reads it
+      // (no LDS DMA builtins, interpolation, GWS or message sends).
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+      asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                   :
+                   : "s"(m0addr), "v"(voff[j]), "s"(j < QA ? rA : rB), "s"(soff)
+                   : "m0");
+#pragma clang diagnostic pop
+    }
+  };
+  // Every wave waits for its own DMAs of the next tile (all but the (NS - 2) Q
+  // youngest, or all of them near the end of K) and for its LDS reads; the
+  // barrier then makes the tile visible and frees the stage read before it.
+  auto sync = [&](bool drain) {
+    if (drain) __builtin_amdgcn_s_waitcnt(FD_VMCNT(0));
+    else __builtin_amdgcn_s_waitcnt(FD_VMCNT((NS - 2) * Q));
+    __builtin_amdgcn_s_waitcnt(FD_LGKMCNT0);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
 
   f32x16 acc[FM][FN];
 #pragma unroll
@@ -229,19 +303,21 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int lr = lane & 31, lk = lane >> 5;
-  // MFMA operand fragments of one 16-wide k-step, double-buffered so that the
-  // LDS reads of step ks + 1 are in flight while the MFMAs of step ks run.
+  const int lr = lane & 31, lk = lane >> 5, xr = (lr >> 2) & 3;
+  // slot of fragment row (A: wm0 + lr, W: BM + wn0 + lr) at k-step ks: K-chunk 2 ks + lk
+  const int ia0 = (wm0 + lr) * 4 + (lk ^ xr), ia1 = (wm0 + lr) * 4 + ((2 + lk) ^ xr);
+  const int ib0 = (BM + wn0 + lr) * 4 + (lk ^ xr), ib1 = (BM + wn0 + lr) * 4 + ((2 + lk) ^ xr);
   V fa[2][FM], fb[2][FN];
-  auto load_frags = [&](int slot, int buf, int ks) {
+  auto load_frags = [&](int slot, int st, int ks) {
+    const uint4* sb = lds + st * STAGE;
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
-      const uint4 v = As(buf)[swz(wm0 + i * 32 + lr, 2 * ks + lk)];
+      const uint4 v = sb[(ks ? ia1 : ia0) + i * 128];
       fa[slot][i] = *reinterpret_cast<const V*>(&v);
     }
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
-      const uint4 v = Bs(buf)[swz(wn0 + j * 32 + lr, 2 * ks + lk)];
+      const uint4 v = sb[(ks ? ib1 : ib0) + j * 128];
       fb[slot][j] = *reinterpret_cast<const V*>(&v);
     }
   };
@@ -251,137 +327,61 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
 #pragma unroll
       for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::run(fa[slot][i], fb[slot][j], acc[i][j]);
   };
-  // One K tile from LDS buffer `buf`; `mid` runs between k-steps 1 and 2.
-  auto compute_tile = [&](int buf, auto mid) {
-    load_frags(0, buf, 0);
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      if (ks + 1 < BK / 16) {
-        load_frags((ks + 1) & 1, buf, ks + 1);
-        // issue the next step's LDS reads ahead of this step's MFMAs
-        __builtin_amdgcn_sched_group_barrier(0x100, FM + FN, 0);
-      }
-      mfmas(ks & 1);
-      __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
-      if (ks == 1) mid();
-    }
-  };
-  auto compute = [&](int buf) { compute_tile(buf, [] {}); };
 
-  const int KT = K / BK;
-  if constexpr (C::PF == 2) {
-    // two register stages: tile kt + 2 is in flight while tile kt is computed;
-    // two K tiles per trip so that the stages have static names
-    FD_GLOAD(ra0, rb0, 0);
-    if (KT > 1) FD_GLOAD(ra1, rb1, 1);
-    FD_LSTORE(ra0, rb0, 0);
-    __syncthreads();
-    for (int kt = 0; kt < KT; kt += 2) {
-      if (kt + 2 < KT) FD_GLOAD(ra0, rb0, kt + 2);
-      compute(0);
-      if (kt + 1 < KT) FD_LSTORE(ra1, rb1, 1);
-      __syncthreads();
-      if (kt + 1 >= KT) break;
-      if (kt + 3 < KT) FD_GLOAD(ra1, rb1, kt + 3);
-      compute(1);
-      if (kt + 2 < KT) FD_LSTORE(ra0, rb0, 0);
-      __syncthreads();
-    }
-  } else {
-    // one register stage: tile kt + 1 is loaded while tile kt is computed, and
-    // written to the other LDS buffer (free since the last barrier) halfway
-    // through and at the end of the MFMA work, so the stores overlap MFMA
-    FD_GLOAD(ra0, rb0, 0);
-    FD_LSTORE(ra0, rb0, 0);
-    __syncthreads();
-    for (int kt = 0; kt < KT; ++kt) {
-      const int cur = kt & 1, nxt = cur ^ 1;
-      const bool more = kt + 1 < KT;
-      if (more) FD_GLOAD(ra0, rb0, kt + 1);
-      compute_tile(cur, [&] {
-        if (more) {
-          _Pragma("unroll") for (int i = 0; i < CA; ++i) As(nxt)[lds_w + i * NT] = ra0[i];
-        }
-      });
-      if (more) {
-        _Pragma("unroll") for (int i = 0; i < CB; ++i) Bs(nxt)[lds_w + i * NT] = rb0[i];
-      }
-      __syncthreads();
-    }
+  // Tile t sits in stage t % NS. The loop starts at the barrier (whose
+  // explicit lgkmcnt(0) leaves no LDS read pending at the loop header), then
+  // reads k-step 0 of tile t + 1, multiplies k-step 1 of tile t, reads k-step 1
+  // of tile t + 1, refills the stage of tile t (read by everyone before the
+  // barrier) with tile t + NS, and multiplies k-step 0 of tile t + 1.
+  const int KT = K / BKD;
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < KT) dma(p, p);
+  sync(KT < NS - 1);
+  load_frags(0, 0, 0);
+  load_frags(1, 0, 1);
+  if (NS - 1 < KT) dma(NS - 1, NS - 1);
+  mfmas(0);
+  int sc = 0;  // stage of tile t
+  for (int t = 0; t < KT - 1; ++t) {
+    const int sn = sc + 1 == NS ? 0 : sc + 1;
+    sync(t + NS - 1 >= KT);
+    load_frags(0, sn, 0);
+    mfmas(1);
+    load_frags(1, sn, 1);
+    if (t + NS < KT) dma(sc, t + NS);
+    mfmas(0);
+    sc = sn;
   }
-#undef FD_GLOAD
-#undef FD_LSTORE
-
-  // epilogue: lane holds column (lane & 31) of each 32x32 block and rows
-  // 8 (r / 4) + 4 (lane / 32) + r % 4
-  if constexpr (EPI == EPI_SWIGLU) {
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm0 + i * 32 + 8 * (r >> 2) + 4 * lk + (r & 3);
-        if (row >= M) continue;
-#pragma unroll
-        for (int j = 0; j < FN; j += 2) {
-          const int pc = n0 + wn0 + j * 32 + lr;  // packed gate column; up is +32
-          if (pc >= N) continue;
-          const float g = acc[i][j][r] + ep.bias[pc];
-          const float u = acc[i][j + 1][r] + ep.bias[pc + 32];
-          const int oc = (n0 + wn0 + j * 32) / 2 + lr;
-          ((T*)ep.out_a)[(int64_t)row * ep.ld_out + oc] = to_act<T>(silu_f(g) * u);
-        }
-      }
-  } else {
-    int64_t coff[FN];
-    float cb[FN];
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int col = min(n0 + wn0 + j * 32 + lr, N - 1);
-      coff[j] = col_off<EPI>(ep, col);
-      cb[j] = ep.bias[col];
-    }
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm0 + i * 32 + 8 * (r >> 2) + 4 * lk + (r & 3);
-        if (row >= M) continue;
-        const int64_t ro = row_off<EPI>(ep, row);
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          if (n0 + wn0 + j * 32 + lr < N) epi_store<EPI, T>(ep, ro + coff[j], acc[i][j][r] + cb[j]);
-      }
-  }
+  mfmas(1);
+  store_tile<EPI, T, FM, FN>(ep, acc, m0 + wm0, n0 + wn0, M, N, lr, lk);
 }
 
 template <typename T, class C, int EPI>
-hipError_t launch_mfma(const GemmArgs& g, hipStream_t s) {
+hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   const int tm = (g.M + C::BM - 1) / C::BM, tn = (g.N + C::BN - 1) / C::BN;
-  static bool attr_set = false;  // raise the dynamic LDS limit once per instantiation
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemm_mfma_kernel<T, C, EPI>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  hipLaunchKernelGGL((gemm_mfma_kernel<T, C, EPI>), dim3(tm * tn), dim3(C::NT), C::LDS_BYTES, s,
+  hipLaunchKernelGGL((gemm_mfma_kernel<T, C, EPI>), dim3(tm * tn), dim3(C::NT), 0, s,
                      (const T*)g.A, (const T*)g.W, g.M, g.N, g.K, g.lda, g.ldw, g.ep, tm, tn);
   return hipGetLastError();
 }
 
-// Tile choice. 256 x 256 tiles load half the bytes per flop of 128 x 128 ones
-// (128 vs 64 flop/byte), which keeps the 256 CUs within L2 bandwidth, but the
-// decoder's small-M projections (M = 3600 rows per 720p frame, N = 1536 or
-// 1920) give only 90-120 such tiles for 256 CUs; there 128 x 128 tiles (two
-// workgroups per CU) are faster. Threshold measured on the 480p / 720p shapes.
-using TileBig = TileCfg<256, 256, 4, 2, 1>;    // 8 waves of 64 x 128, one workgroup per CU
-using TileSmall = TileCfg<128, 128, 2, 2, 2>;  // 4 waves of 64 x 64, two workgroups per CU
+// Tile choice, measured on the 480p / 720p decoder shapes. 256 x 256 tiles
+// (8 waves of 128 x 64) read the fewest LDS and L2 bytes per flop and win where
+// there are enough of them to fill the 256 CUs. The small-M backbone
+// projections (M = 3600 rows per 720p frame, N = 1536 or 1920) give only 90-120
+// such tiles; there, and for residual-add epilogues behind a short K loop
+// (whose read-modify-write of the fp32 stream is a large share of the time),
+// 128 x 128 tiles win: several workgroups share a CU, so one's epilogue and
+// barriers overlap another's MFMAs.
+using TileL = TileCfg<256, 256, 2, 4, 4>;  // 8 waves of 128 x 64, one workgroup per CU
+using TileS = TileCfg<128, 128, 2, 2, 3>;  // 4 waves of 64 x 64, two or more per CU
 
 template <typename T, int EPI>
 hipError_t dispatch_tiles(const GemmArgs& g, hipStream_t s) {
-  const int tiles_big = ((g.M + 255) / 256) * ((g.N + 255) / 256);
-  if (tiles_big >= 160) return launch_mfma<T, TileBig, EPI>(g, s);
-  return launch_mfma<T, TileSmall, EPI>(g, s);
+  const int tiles_l = ((g.M + 255) / 256) * ((g.N + 255) / 256);
+  const bool short_rmw = EPI == EPI_RESID_ADD && g.K <= 2048;
+  if (tiles_l >= 160 && !short_rmw) return launch_gemm<T, TileL, EPI>(g, s);
+  return launch_gemm<T, TileS, EPI>(g, s);
 }
 
 template <typename T>
@@ -460,7 +460,7 @@ hipError_t launch_f32(const GemmArgs& g, hipStream_t s) {
 
 hipError_t gemm_mfma(Act16 t, const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
-  if (g.K % BK || g.lda % 8 || g.ldw % 8) return hipErrorInvalidValue;
+  if (g.K <= 0 || g.K % BKD || g.lda % 8 || g.ldw % 8) return hipErrorInvalidValue;
   if (g.epi == EPI_SWIGLU && g.N % 64) return hipErrorInvalidValue;
   return t == Act16::F16 ? dispatch_epi<_Float16>(g, s) : dispatch_epi<__hip_bfloat16>(g, s);
 }

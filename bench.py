@@ -9,6 +9,14 @@ inputs are seeded synthetic latents and N(0, 0.02) weights, resident in HBM
 before timing starts. Prints one JSON line.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+  python bench.py --copy-calibration MIB   (plain device copy of MIB MiB, for
+                                            scaling HBM byte counters)
+
+The roofline's "traffic" (HBM bytes per launch of the roofline kernel) comes
+from two rocprofv3 counter passes (FETCH_SIZE, WRITE_SIZE) over this script,
+scaled by what the same counters read for the plain copy; the figures are kept
+in profiles/ together with the SHA-256 of the kernel source they were taken on,
+and reported only while that source is unchanged.
 """
 from __future__ import annotations
 
@@ -23,6 +31,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_F16_TFLOPS = 2500.0   # MI355X dense fp16 / bf16 MFMA
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_refine_xl720p_traffic.md")
+ATTN_SOURCE = os.path.join(ROOT, "paper_2607_14898_amd", "csrc", "k_attn.hip")
 METRIC = "decoded frames/sec at 720p (latent->pixel), p50 per-chunk latency, % MFMA peak"
 
 
@@ -72,6 +82,38 @@ def cpu_baseline(wl, weights, gpu_fps_unit_flops):
             "cpu": platform.processor() or platform.machine()}
 
 
+def counter_traffic():
+    """HBM bytes per launch of the refinement attention from the committed
+    counter summary, or None if it is missing or was taken on other source."""
+    import hashlib
+    try:
+        fields = {}
+        for line in open(TRAFFIC_FILE):
+            if line.startswith("    ") and ":" in line:
+                k, v = line.strip().split(":", 1)
+                fields[k.strip()] = v.strip()
+        src = hashlib.sha256(open(ATTN_SOURCE, "rb").read()).hexdigest()
+        if fields.get("kernel_source_sha256") != src:
+            return None
+        return int(fields["hbm_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def copy_calibration(mib: int) -> int:
+    """A plain device-to-device copy of known size: the reference for scaling
+    the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n * 4, "launches": 3}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -79,12 +121,15 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default="xl-720p-stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, metavar="MIB")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(see DESIGN.md for how the decoder would shard); run with --gpus 1.",
               file=sys.stderr)
         return 2
+    if args.copy_calibration:
+        return copy_calibration(args.copy_calibration)
 
     import numpy as np
     import torch
@@ -173,7 +218,7 @@ def main() -> int:
             "peak": PEAK_F16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_F16_TFLOPS, 4),
-            "traffic": None,
+            "traffic": counter_traffic(),
             "launches": attn_n,
             "avg_launch_us": round(attn_ms * 1e3 / max(attn_n, 1), 2),
         },

@@ -14,10 +14,12 @@
 // sums stay lane-local (v_dot2 over the f16 probabilities) until the end. K
 // rows are fed to the MFMA in the order that makes the score registers of a
 // lane exactly the B operand of the following O^T += V^T P^T MFMA, so P never
-// leaves registers. The scale folds into the exp2 argument (one FMA per
-// score), the running max is only raised when it grows by more than 2^8
-// (the accumulators are rescaled then, rarely), and only the ragged last tile
-// of a unit is masked. K and V^T tiles of 64 keys are double-buffered in LDS.
+// leaves registers. Queries are pre-scaled by log2(e) / sqrt(D_h), and one
+// extra MFMA k-step subtracts each query's running shift, so the MFMA output
+// is the exp2 argument itself. The shift is raised (and O and the row sum
+// rescaled) only on the first tile and when some probability of a lane could
+// leave the f16 range; only the ragged last tile of a unit is masked. K and
+// V^T tiles of 64 keys are double-buffered in LDS.
 #include "fd_kernels.h"
 
 #include <hip/hip_bf16.h>

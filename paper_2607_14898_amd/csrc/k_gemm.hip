@@ -154,10 +154,21 @@ __device__ __forceinline__ void tile_of(int bid, int n_tiles, int tiles_m, int t
 // Epilogue of one wave's FM x FN blocks of 32 x 32 accumulators whose first
 // output row / column are r0 / c0. MFMA accumulator layout: lane (lk, lr) holds
 // column lr of each block and rows 8 (r / 4) + 4 lk + r % 4 for r = 0..15.
+// Loads of the destination (residual add) are issued for a whole 32-row block
+// before any of its stores: interleaved, every load would wait for the store
+// before it (the compiler cannot tell the addresses apart) and each element
+// would cost a full memory round trip.
 template <int EPI, typename T, int FM, int FN>
 __device__ __forceinline__ void store_tile(const EpiParams& ep, const f32x16 (&acc)[FM][FN], int r0,
                                            int c0, int M, int N, int lr, int lk) {
   if constexpr (EPI == EPI_SWIGLU) {
+    float bg[FN / 2], bu[FN / 2];
+#pragma unroll
+    for (int j = 0; j < FN; j += 2) {
+      const int pc = min(c0 + j * 32 + lr, N - 33);  // packed gate column; up is +32
+      bg[j / 2] = ep.bias[pc];
+      bu[j / 2] = ep.bias[pc + 32];
+    }
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -166,10 +177,9 @@ __device__ __forceinline__ void store_tile(const EpiParams& ep, const f32x16 (&a
         if (row >= M) continue;
 #pragma unroll
         for (int j = 0; j < FN; j += 2) {
-          const int pc = c0 + j * 32 + lr;  // packed gate column; up is +32
-          if (pc >= N) continue;
-          const float g = acc[i][j][r] + ep.bias[pc];
-          const float u = acc[i][j + 1][r] + ep.bias[pc + 32];
+          if (c0 + j * 32 + lr >= N) continue;
+          const float g = acc[i][j][r] + bg[j / 2];
+          const float u = acc[i][j + 1][r] + bu[j / 2];
           const int oc = (c0 + j * 32) / 2 + lr;
           ((T*)ep.out_a)[(int64_t)row * ep.ld_out + oc] = to_act<T>(silu_f(g) * u);
         }
@@ -177,23 +187,43 @@ __device__ __forceinline__ void store_tile(const EpiParams& ep, const f32x16 (&a
   } else {
     int64_t coff[FN];
     float cb[FN];
+    bool cok[FN];
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       const int col = min(c0 + j * 32 + lr, N - 1);
       coff[j] = col_off<EPI>(ep, col);
       cb[j] = ep.bias[col];
+      cok[j] = c0 + j * 32 + lr < N;
     }
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < FM; ++i) {
+      int64_t ro[16];
+      bool rok[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = r0 + i * 32 + 8 * (r >> 2) + 4 * lk + (r & 3);
-        if (row >= M) continue;
-        const int64_t ro = row_off<EPI>(ep, row);
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          if (c0 + j * 32 + lr < N) epi_store<EPI, T>(ep, ro + coff[j], acc[i][j][r] + cb[j]);
+        rok[r] = row < M;
+        ro[r] = row_off<EPI>(ep, min(row, M - 1));
       }
+      if constexpr (EPI == EPI_RESID_ADD) {
+        float old[16][FN];
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+#pragma unroll
+          for (int j = 0; j < FN; ++j) old[r][j] = rok[r] && cok[j] ? ep.out_f[ro[r] + coff[j]] : 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            if (rok[r] && cok[j]) ep.out_f[ro[r] + coff[j]] = old[r][j] + (acc[i][j][r] + cb[j]);
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            if (rok[r] && cok[j]) epi_store<EPI, T>(ep, ro[r] + coff[j], acc[i][j][r] + cb[j]);
+      }
+    }
   }
 }
 
@@ -365,22 +395,30 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Tile choice, measured on the 480p / 720p decoder shapes. 256 x 256 tiles
-// (8 waves of 128 x 64) read the fewest LDS and L2 bytes per flop and win where
-// there are enough of them to fill the 256 CUs. The small-M backbone
-// projections (M = 3600 rows per 720p frame, N = 1536 or 1920) give only 90-120
-// such tiles; there, and for residual-add epilogues behind a short K loop
-// (whose read-modify-write of the fp32 stream is a large share of the time),
-// 128 x 128 tiles win: several workgroups share a CU, so one's epilogue and
-// barriers overlap another's MFMAs.
-using TileL = TileCfg<256, 256, 2, 4, 4>;  // 8 waves of 128 x 64, one workgroup per CU
-using TileS = TileCfg<128, 128, 2, 2, 3>;  // 4 waves of 64 x 64, two or more per CU
+// Tile choice, measured on the 480p / 720p decoder shapes (random fp16 data).
+// - 256 x 256 tiles (8 waves of 128 x 64) read the fewest LDS and L2 bytes
+//   per flop and win wherever there are enough of them to fill the 256 CUs,
+//   except for residual-add epilogues behind a short K loop.
+// - When 192 x 128 tiles come to one nearly full wave (200-256 workgroups,
+//   the backbone's M = 3600 x N = 1536 projections), one workgroup per CU with
+//   6 stages in flight wins.
+// - When even 128 x 128 tiles leave CUs idle (480p backbone), each CU runs a
+//   single workgroup, so it gets 6 stages in flight.
+// - Otherwise 128 x 128 tiles with 3 stages, several workgroups per CU, so one
+//   workgroup's epilogue and barriers overlap another's MFMAs.
+using TileL = TileCfg<256, 256, 2, 4, 4>;   // 8 waves of 128 x 64, 128 KB LDS
+using TileM = TileCfg<192, 128, 2, 2, 6>;   // 4 waves of 96 x 64, 120 KB
+using TileS1 = TileCfg<128, 128, 2, 2, 6>;  // 4 waves of 64 x 64, 96 KB
+using TileS = TileCfg<128, 128, 2, 2, 3>;   // 4 waves of 64 x 64, 48 KB
 
 template <typename T, int EPI>
 hipError_t dispatch_tiles(const GemmArgs& g, hipStream_t s) {
-  const int tiles_l = ((g.M + 255) / 256) * ((g.N + 255) / 256);
+  auto tiles = [&](int bm, int bn) { return ((g.M + bm - 1) / bm) * ((g.N + bn - 1) / bn); };
   const bool short_rmw = EPI == EPI_RESID_ADD && g.K <= 2048;
-  if (tiles_l >= 160 && !short_rmw) return launch_gemm<T, TileL, EPI>(g, s);
+  if (tiles(256, 256) >= 160 && !short_rmw) return launch_gemm<T, TileL, EPI>(g, s);
+  const int tm = tiles(192, 128);
+  if (tm >= 200 && tm <= 256) return launch_gemm<T, TileM, EPI>(g, s);
+  if (tiles(128, 128) <= 256) return launch_gemm<T, TileS1, EPI>(g, s);
   return launch_gemm<T, TileS, EPI>(g, s);
 }
 

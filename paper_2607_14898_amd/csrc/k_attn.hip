@@ -194,7 +194,12 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
     const bool tail = kt == tiles_per_unit - 1 && tail_valid < KT;
     if (++kt == tiles_per_unit) kt = 0;
     f32x16 s[2][NQB];
+    // The MFMA blocks run at raised wave priority: a wave that reaches its MFMAs
+    // issues them ahead of the other wave on the SIMD, which meanwhile issues its
+    // exp2 / conversion work, so the two waves drift into opposite phases and the
+    // matrix and vector units overlap more.
     auto scores = [&]() {
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
@@ -208,6 +213,7 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
           for (int qb = 0; qb < NQB; ++qb) s[kb][qb] = M::run(kf, qf[qb][ks], s[kb][qb]);
         }
       }
+      __builtin_amdgcn_s_setprio(0);
       if (tail) {  // ragged end of a unit
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
@@ -279,6 +285,7 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
 #pragma unroll
     for (int qb = 0; qb < NQB; ++qb) l_run[qb] += ls[qb];
 
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int d = 0; d < 2; ++d) {
 #pragma unroll
@@ -289,6 +296,7 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
         for (int qb = 0; qb < NQB; ++qb) acc[qb][d] = M::run(vf, pf[qb][st], acc[qb][d]);
       }
     }
+    __builtin_amdgcn_s_setprio(0);
     if (it + 1 < n_it) lstore(cur ^ 1);
     __syncthreads();
   }

@@ -82,8 +82,15 @@ __device__ __forceinline__ int key_of_row(int i) {
 
 constexpr int KT = 64;   // keys per tile
 
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t attn_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
+}
+
 // Workgroup: 4 waves = HPB heads of one KV group x (4 / HPB) query sub-tiles of
-// 64 queries. K and V^T tiles of 64 keys are shared by the 4 waves through LDS.
+// 64 queries. K and V^T tiles of 64 keys are shared by the 4 waves through LDS;
+// they are copied there by buffer-to-LDS DMA (no register staging), one tile
+// ahead. Each wave's Q fragments sit in LDS too, which leaves the registers
+// for reading a whole tile's K fragments ahead of the score MFMAs.
 template <typename T, int HPB, int NQB>
 __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnArgs a, int q_tiles) {
   using M = AMfma<T>;
@@ -92,8 +99,10 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
   constexpr int QB = QW * (4 / HPB);  // queries per workgroup
   __shared__ uint4 sk[2][KT * 8];
   __shared__ uint4 sv[2][KT * 8];
+  __shared__ uint4 sq[4][NQB * 4 * 64];  // Q fragments of each wave, lane order
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 31, lh = lane >> 5;
   const int bx = blockIdx.x;
   const int qt = bx % q_tiles, bu = bx / q_tiles;
@@ -107,19 +116,20 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
 
   // queries pre-scaled by log2(e) / sqrt(D_h): S^T then holds exp2 arguments
   const float c = a.scale * 1.44269504088896341f;
-  V qf[NQB][4];
-  int64_t qrow[NQB];
+  auto qrow = [&](int qb) {
+    return (int64_t)(b * a.n_units + lu) * a.U + min(q0 + qb * 32 + lr, a.U - 1);
+  };
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb) {
-    const int qi = min(q0 + qb * 32 + lr, a.U - 1);
-    qrow[qb] = (int64_t)(b * a.n_units + lu) * a.U + qi;
-    const T* qp = (const T*)a.q + qrow[qb] * ldq + n * 64 + 8 * lh;
+    const T* qp = (const T*)a.q + qrow(qb) * ldq + n * 64 + 8 * lh;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const uint4 v = *reinterpret_cast<const uint4*>(qp + 16 * ks);
       const V raw = *reinterpret_cast<const V*>(&v);
+      V qv;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) qf[qb][ks][e] = M::cvt((float)raw[e] * c);
+      for (int e = 0; e < 8; ++e) qv[e] = M::cvt((float)raw[e] * c);
+      sq[wave][(qb * 4 + ks) * 64 + lane] = *reinterpret_cast<const uint4*>(&qv);
     }
   }
 
@@ -128,39 +138,61 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
   const int n_it = (int)(u - u_lo + 1) * tiles_per_unit;
   const int tail_valid = a.U - (tiles_per_unit - 1) * KT;  // keys in a unit's last tile
 
-  // tile walk: (slot, tile) advanced incrementally
+  // DMA of a tile: wave w moves rows 8 w .. 8 w + 7 and 8 (w + 4) .. of the K
+  // tile and of the V^T tile; lane l lands in row base + l / 8, physical chunk
+  // l % 8, which holds chunk (l % 8) ^ ((row / 2) % 8) (the swizzle of swz_k /
+  // swz_v). The tile walk (ring slot, tile of the unit) advances incrementally.
   int ld_slot = (int)(u_lo % a.S), ld_kt = 0;
   const int64_t ring0 = (int64_t)(b * a.G + g) * a.S;
-  const int c0 = tid, c1 = tid + 256;  // the two 16-byte chunks of each tile this thread moves
-  const int k_off0 = (c0 >> 3) * 64 + (c0 & 7) * 8, k_off1 = (c1 >> 3) * 64 + (c1 & 7) * 8;
-  const int v_off0 = (c0 >> 3) * a.U_pad + (c0 & 7) * 8, v_off1 = (c1 >> 3) * a.U_pad + (c1 & 7) * 8;
-  const int sk0 = swz_k(c0 >> 3, c0 & 7), sk1 = swz_k(c1 >> 3, c1 & 7);
-  const int sv0 = swz_v(c0 >> 3, c0 & 7), sv1 = swz_v(c1 >> 3, c1 & 7);
-  uint4 rk0, rk1, rv0, rv1;
-  auto gload = [&]() {
-    const int64_t ring = ring0 + ld_slot;
-    const T* kb = (const T*)a.k_ring + (ring * a.U_pad + (int64_t)ld_kt * KT) * 64;
-    const T* vb = (const T*)a.vt_ring + ring * 64 * a.U_pad + (int64_t)ld_kt * KT;
-    rk0 = *reinterpret_cast<const uint4*>(kb + k_off0);
-    rk1 = *reinterpret_cast<const uint4*>(kb + k_off1);
-    rv0 = *reinterpret_cast<const uint4*>(vb + v_off0);
-    rv1 = *reinterpret_cast<const uint4*>(vb + v_off1);
+  const __amdgpu_buffer_rsrc_t rk =
+      attn_rsrc((const T*)a.k_ring + ring0 * a.U_pad * 64, (uint32_t)a.S * a.U_pad * 128u);
+  const __amdgpu_buffer_rsrc_t rv =
+      attn_rsrc((const T*)a.vt_ring + ring0 * 64 * a.U_pad, (uint32_t)a.S * 64u * a.U_pad * 2u);
+  const uint32_t ldsk0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint4*)&sk[0][0];
+  const uint32_t ldsv0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint4*)&sv[0][0];
+  auto dma_tile = [&](int buf) {
+    const uint32_t sofk = (uint32_t)(ld_slot * a.U_pad + ld_kt * KT) * 128u;
+    const uint32_t sofv = (uint32_t)ld_slot * 64u * (uint32_t)a.U_pad * 2u + (uint32_t)ld_kt * KT * 2u;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int rb = 8 * (wave + 4 * h);  // first row of this DMA
+      int l = __builtin_amdgcn_workitem_id_x() & 63;
+      const int row = rb + (l >> 3), ch = (l & 7) ^ ((row >> 1) & 7);
+      const uint32_t vk = (uint32_t)(row * 128 + ch * 16);
+      const uint32_t vv = (uint32_t)(row * a.U_pad * 2 + ch * 16);
+      const uint32_t bo = (uint32_t)buf * KT * 8 * 16 + (uint32_t)rb * 8 * 16;
+      // M0 is reserved by the compiler, but nothing else in this kernel reads it.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+      asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                   :
+                   : "s"(ldsk0 + bo), "v"(vk), "s"(rk), "s"(sofk)
+                   : "m0");
+      asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                   :
+                   : "s"(ldsv0 + bo), "v"(vv), "s"(rv), "s"(sofv)
+                   : "m0");
+#pragma clang diagnostic pop
+    }
     if (++ld_kt == tiles_per_unit) {
       ld_kt = 0;
       if (++ld_slot == a.S) ld_slot = 0;
     }
   };
-  auto lstore = [&](int buf) {
-    sk[buf][sk0] = rk0;
-    sk[buf][sk1] = rk1;
-    sv[buf][sv0] = rv0;
-    sv[buf][sv1] = rv1;
+  // end of a tile: this wave's DMAs and LDS reads are complete, then the
+  // barrier publishes the next tile and frees the buffer just read
+  auto sync = [&]() {
+    __builtin_amdgcn_s_waitcnt(0);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
   };
 
   // Running shift m_q of each query, kept as an f16 value: an extra 16-wide
-  // k-step multiplies the constant column (1, 0, ..., 0) of K with (-m_q, 0, ..)
-  // of Q, so the MFMA returns c q.k - m_q exactly and P = exp2(S^T) needs no
-  // VALU work before the exponential. The shift only has to keep P in f16
+  // k-step multiplies the constant columns (1, mask, 0, ..., 0) of K with
+  // (-m_q, 1, 0, ...) of Q, so the MFMA returns c q.k - m_q (and -60000 more
+  // for the padding keys of a ragged tile) and P = exp2(S^T) needs no VALU
+  // work before the exponential. The shift only has to keep P in f16
   // range: it is raised (and O, l rescaled by the exact exp2 of the change of
   // the f16 shifts) on the first tile and whenever some p of a lane may exceed
   // 2^15, detected from the lane's partial row sum of the tile.
@@ -169,7 +201,7 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
   for (int e = 0; e < 8; ++e) {
     kone[e] = M::cvt(e == 0 && lh == 0 ? 1.f : 0.f);
 #pragma unroll
-    for (int qb = 0; qb < NQB; ++qb) mqf[qb][e] = M::cvt(0.f);
+    for (int qb = 0; qb < NQB; ++qb) mqf[qb][e] = M::cvt(e == 1 && lh == 0 ? 1.f : 0.f);
   }
   float mq[NQB], l_run[NQB];
 #pragma unroll
@@ -182,13 +214,12 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[qb][d][r] = 0.f;
 
-  gload();
-  lstore(0);
-  __syncthreads();
+  dma_tile(0);
+  sync();
   int kt = 0;
   for (int it = 0; it < n_it; ++it) {
     const int cur = it & 1;
-    if (it + 1 < n_it) gload();
+    if (it + 1 < n_it) dma_tile(cur ^ 1);
 
     // S^T = K Q^T - m_q: lane holds query lr of each 32-query block, 16 keys per key block
     const bool tail = kt == tiles_per_unit - 1 && tail_valid < KT;
@@ -199,33 +230,34 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
     // exp2 / conversion work, so the two waves drift into opposite phases and the
     // matrix and vector units overlap more.
     auto scores = [&]() {
+      // all K fragments of the tile are read before the first MFMA
+      V kfr[2][4];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+          const uint4 v = sk[cur][swz_k(kb * 32 + key_of_row(lr), 2 * ks + lh)];
+          kfr[kb][ks] = *reinterpret_cast<const V*>(&v);
+        }
       __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
+        // second column of the constant K operand: -60000 on the padding keys
+        // of a unit's ragged last tile, so exp2 of their scores is 0
+        V ka = kone;
+        ka[1] = M::cvt(tail && lh == 0 && kb * 32 + key_of_row(lr) >= tail_valid ? -60000.f : 0.f);
 #pragma unroll
-        for (int qb = 0; qb < NQB; ++qb) s[kb][qb] = M::run(kone, mqf[qb], f32x16{});
-        const int krow = kb * 32 + key_of_row(lr);
+        for (int qb = 0; qb < NQB; ++qb) s[kb][qb] = M::run(ka, mqf[qb], f32x16{});
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
-          const uint4 v = sk[cur][swz_k(krow, 2 * ks + lh)];
-          const V kf = *reinterpret_cast<const V*>(&v);
 #pragma unroll
-          for (int qb = 0; qb < NQB; ++qb) s[kb][qb] = M::run(kf, qf[qb][ks], s[kb][qb]);
+          for (int qb = 0; qb < NQB; ++qb) {
+            const uint4 w = sq[wave][(qb * 4 + ks) * 64 + lane];
+            s[kb][qb] = M::run(kfr[kb][ks], *reinterpret_cast<const V*>(&w), s[kb][qb]);
+          }
         }
       }
       __builtin_amdgcn_s_setprio(0);
-      if (tail) {  // ragged end of a unit
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = kb * 32 + 16 * (r >> 3) + 8 * lh + (r & 7);
-            if (key >= tail_valid) {
-#pragma unroll
-              for (int qb = 0; qb < NQB; ++qb) s[kb][qb][r] = -INFINITY;
-            }
-          }
-      }
     };
     // P = exp2(S^T) in f16, laid out as the B operand of O^T += V^T P^T
     V pf[NQB][4];
@@ -297,8 +329,7 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
       }
     }
     __builtin_amdgcn_s_setprio(0);
-    if (it + 1 < n_it) lstore(cur ^ 1);
-    __syncthreads();
+    sync();
   }
 
 #pragma unroll
@@ -306,7 +337,7 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
     const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
     const float inv = 1.f / l_tot;
     if (q0 + qb * 32 + lr < a.U) {
-      T* op = (T*)a.o + qrow[qb] * ldq + n * 64;
+      T* op = (T*)a.o + qrow(qb) * ldq + n * 64;
 #pragma unroll
       for (int d = 0; d < 2; ++d)
 #pragma unroll

@@ -40,13 +40,23 @@ struct EpiParams {
 
 struct GemmArgs {
   const void* A = nullptr;  // [M, K] row-major, lda
-  const void* W = nullptr;  // [N, K] row-major, ldw
+  // [N, K]: row-major with stride ldw for the fp32 GEMM; for the 16-bit MFMA
+  // GEMM packed K-tile-major (see pack_w16_index), ldw = K
+  const void* W = nullptr;
   int M = 0, N = 0, K = 0, lda = 0, ldw = 0;
   Epi epi = EPI_STORE_F32;
   EpiParams ep;
 };
 
-// 16-bit operand GEMM on MFMA (K > 0, K % 32 == 0, lda/ldw % 8 == 0, 16-byte aligned).
+// Position of element (row, k) of an [N, K] weight in the packed layout the
+// 16-bit MFMA GEMM reads: 1 KB blocks of 16 rows x 32 K-columns, block-row
+// major, rows padded with zeros to a multiple of 16 (ceil(N / 16) 16 K
+// elements in all).
+inline int64_t pack_w16_index(int64_t row, int64_t k, int64_t K) {
+  return ((row / 16) * (K / 32) + k / 32) * 512 + (row % 16) * 32 + k % 32;
+}
+// 16-bit operand GEMM on MFMA (K > 0, K % 32 == 0, lda % 8 == 0, 16-byte aligned
+// A; W packed as above).
 hipError_t gemm_mfma(Act16 t, const GemmArgs& g, hipStream_t stream);
 // fp32 GEMM (any shape) for the fp32 compute path.
 hipError_t gemm_f32(const GemmArgs& g, hipStream_t stream);

@@ -540,10 +540,13 @@ fd_status upload_weights(fd_decoder* dec, const void* w, int32_t wdt, size_t n_e
   for (auto& t : specs) total += (size_t)t.s0 * (t.ndim == 2 ? t.s1 : 1);
   if (n_elems != total)
     return fail(FD_ERR_INVALID_ARGUMENT, "weight blob has %zu elements, layout needs %zu", n_elems, total);
-  // device sizes: matrices in the compute type (packed), vectors in fp32
+  // device sizes: matrices in the compute type, vectors in fp32; 16-bit
+  // matrices are stored K-tile-major for the MFMA GEMM (fd::pack_w16_index),
+  // rows padded to a multiple of 16
+  auto mat_k = [&](const TensorSpec& t) -> int64_t { return t.name == "embed.w" ? d.K_pad : t.s1; };
   auto mat_elems = [&](const TensorSpec& t) -> size_t {
-    if (t.name == "embed.w") return (size_t)t.s0 * d.K_pad;
-    return (size_t)t.s0 * t.s1;
+    const int64_t rows = d.is16 ? (t.s0 + 15) / 16 * 16 : t.s0;
+    return (size_t)rows * mat_k(t);
   };
   size_t wbytes = 0, fbytes = 0;
   for (auto& t : specs) {
@@ -595,9 +598,17 @@ fd_status upload_weights(fd_decoder* dec, const void* w, int32_t wdt, size_t n_e
     if (t.ndim == 2) {
       size_t elems = mat_elems(t);
       if (t.name == "embed.w" && d.K_pad != t.s1) {
-        host.assign(elems, 0.f);
+        host.assign((size_t)t.s0 * d.K_pad, 0.f);
         for (int64_t r = 0; r < t.s0; ++r)
           std::memcpy(&host[r * d.K_pad], &src[r * t.s1], t.s1 * 4);
+        src.swap(host);
+      }
+      if (d.is16) {  // K-tile-major packing (zero rows up to a multiple of 16)
+        const int64_t K = mat_k(t);
+        host.assign(elems, 0.f);
+        for (int64_t r = 0; r < t.s0; ++r)
+          for (int64_t k = 0; k < K; k += 32)  // runs of 32 K-columns stay contiguous
+            std::memcpy(&host[fd::pack_w16_index(r, k, K)], &src[r * K + k], 32 * sizeof(float));
         src.swap(host);
       }
       if (d.is16) {

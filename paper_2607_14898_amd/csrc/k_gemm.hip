@@ -282,10 +282,17 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
   const int m0 = tm * BM, n0 = tn * BN;
   const int wm0 = (wave / C::WAVES_N) * C::WM, wn0 = (wave % C::WAVES_N) * C::WN;
 
+  // A is row-major (lda). W is packed K-tile-major: blocks of 16 rows x 32
+  // K-columns (1 KB), block (row / 16, k / 32) at ((row / 16) (K / 32) + k / 32) KB,
+  // rows padded with zeros to a multiple of 16, so each DMA of W reads one
+  // contiguous 1 KB block.
+  const int KB = K / BKD;  // K tiles
   const __amdgpu_buffer_rsrc_t rA =
       make_rsrc(A + (int64_t)m0 * lda, (uint32_t)min(BM, M - m0) * lda * (uint32_t)sizeof(T));
+  const int nrows_w = min(BN, (N + 15) / 16 * 16 - n0);
   const __amdgpu_buffer_rsrc_t rB =
-      make_rsrc(W + (int64_t)n0 * ldw, (uint32_t)min(BN, N - n0) * ldw * (uint32_t)sizeof(T));
+      make_rsrc(W + (int64_t)(n0 / 16) * KB * 512, (uint32_t)(nrows_w / 16) * KB * 1024u);
+  (void)ldw;
   // DMA j of this wave fills stage rows 16 q .. 16 q + 15, q = j NW + wave (A
   // rows for j < QA, W rows after); lane l lands in row 16 q + l / 4, physical
   // chunk l % 4, which holds K-chunk (l % 4) ^ ((l / 16) % 4).
@@ -293,14 +300,16 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
   uint32_t voff[Q];
 #pragma unroll
   for (int j = 0; j < Q; ++j) {
-    const int row = 16 * (j * NW + wave) + lrow - (j < QA ? 0 : BM);
-    voff[j] = (uint32_t)(row * (j < QA ? lda : ldw) + lchunk * 8) * (uint32_t)sizeof(T);
+    const int q = j * NW + wave;
+    voff[j] = j < QA ? (uint32_t)((16 * q + lrow) * lda + lchunk * 8) * (uint32_t)sizeof(T)
+                     : (uint32_t)(q - BM / 16) * KB * 1024u + (uint32_t)(lrow * 64 + lchunk * 16);
   }
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint4*)lds;
   auto dma = [&](int st, int kt) {
-    const uint32_t soff = (uint32_t)kt * BKD * (uint32_t)sizeof(T);
+    const uint32_t soffA = (uint32_t)kt * BKD * (uint32_t)sizeof(T), soffB = (uint32_t)kt * 1024u;
 #pragma unroll
     for (int j = 0; j < Q; ++j) {
+      const uint32_t soff = j < QA ? soffA : soffB;
       const uint32_t m0addr = lds0 + (uint32_t)(st * STAGE + 64 * (j * NW + wave)) * 16u;
       // M0 is reserved by the compiler, but nothing else in this kernel reads it
       // (no LDS DMA builtins, interpolation, GWS or message sends).
@@ -498,7 +507,7 @@ hipError_t launch_f32(const GemmArgs& g, hipStream_t s) {
 
 hipError_t gemm_mfma(Act16 t, const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
-  if (g.K <= 0 || g.K % BKD || g.lda % 8 || g.ldw % 8) return hipErrorInvalidValue;
+  if (g.K <= 0 || g.K % BKD || g.lda % 8 || g.ldw != g.K) return hipErrorInvalidValue;
   if (g.epi == EPI_SWIGLU && g.N % 64) return hipErrorInvalidValue;
   return t == Act16::F16 ? dispatch_epi<_Float16>(g, s) : dispatch_epi<__hip_bfloat16>(g, s);
 }

@@ -20,7 +20,31 @@ enum Epi : int {
   EPI_TUP = 6,         // temporal upsampling reshape into the refinement stream (fp32)
   EPI_PIXEL = 7,       // head output -> PixelShuffle store (+clamp), fp32 pixels
   EPI_LINEAR_PIXEL = 8,// linear head output -> sub-frame + PixelShuffle store
-  EPI_COUNT = 9
+  EPI_QKV = 9,         // KV-norm + 3D-RoPE of the QKV projection: q buffer and K / V^T rings
+  EPI_COUNT = 10
+};
+
+struct QkvPostArgs {
+  const float* raw = nullptr;  // [rows, D + 2 G D_h]
+  void* q = nullptr;           // [rows, N D_h]
+  void* k_ring = nullptr;
+  void* vt_ring = nullptr;
+  const float* knorm_g = nullptr;  // [D_h] or null
+  const float* vnorm_g = nullptr;
+  const int* rope_axis = nullptr;  // [D_h / 2] axis of each pair (0 t, 1 h, 2 w)
+  const double* rope_freq = nullptr;// [D_h / 2] angular frequency of each pair
+  const float2* rope_hw = nullptr;  // [max(grid_h, grid_w)][D_h / 2] (cos, sin) of spatial pairs
+  float2* rope_t = nullptr;         // [(sub-)frames of the call][D_h / 2] temporal (cos, sin), filled here
+  int rope = 1;
+  float eps = 1e-6f;
+  int B = 1, N = 1, G = 1, Dh = 64;
+  int rows_per_batch = 0;      // rows of one stream in this call
+  int L = 0;                   // tokens per (sub-)frame
+  int grid_w = 1;
+  int U = 0, U_pad = 0, S = 1; // unit geometry of the ring
+  int64_t u0 = 0;              // absolute index of the first unit of the call
+  int64_t tau0 = 0;            // temporal position of the call's first (sub-)frame
+  int out_kind = 0;            // 0 f16, 1 bf16, 2 fp32
 };
 
 struct EpiParams {
@@ -36,6 +60,7 @@ struct EpiParams {
   int frames_in = 0;        // latent frames in the call
   int frames_out = 0;       // output frames in the call (frames_in * r_t)
   int clamp = 1;
+  QkvPostArgs qkv;          // EPI_QKV geometry and destinations (raw unused)
 };
 
 struct GemmArgs {
@@ -85,29 +110,10 @@ hipError_t norm_rows(const float* x, int M, int D, const float* g, const float* 
 
 // Split raw qkv (fp32, bias included) into rotated queries and the KV ring
 // (KV-norm, RoPE) for rows of one call.
-struct QkvPostArgs {
-  const float* raw = nullptr;  // [rows, D + 2 G D_h]
-  void* q = nullptr;           // [rows, N D_h]
-  void* k_ring = nullptr;
-  void* vt_ring = nullptr;
-  const float* knorm_g = nullptr;  // [D_h] or null
-  const float* vnorm_g = nullptr;
-  const int* rope_axis = nullptr;  // [D_h / 2] axis of each pair (0 t, 1 h, 2 w)
-  const double* rope_freq = nullptr;// [D_h / 2] angular frequency of each pair
-  const float2* rope_hw = nullptr;  // [max(grid_h, grid_w)][D_h / 2] (cos, sin) of spatial pairs
-  float2* rope_t = nullptr;         // [(sub-)frames of the call][D_h / 2] temporal (cos, sin), filled here
-  int rope = 1;
-  float eps = 1e-6f;
-  int B = 1, N = 1, G = 1, Dh = 64;
-  int rows_per_batch = 0;      // rows of one stream in this call
-  int L = 0;                   // tokens per (sub-)frame
-  int grid_w = 1;
-  int U = 0, U_pad = 0, S = 1; // unit geometry of the ring
-  int64_t u0 = 0;              // absolute index of the first unit of the call
-  int64_t tau0 = 0;            // temporal position of the call's first (sub-)frame
-  int out_kind = 0;            // 0 f16, 1 bf16, 2 fp32
-};
 hipError_t qkv_post(const QkvPostArgs& a, hipStream_t stream);
+// Temporal (cos, sin) of the call's (sub-)frames into a.rope_t; run once per
+// stack and call, before the QKV post step of its layers.
+hipError_t rope_time(const QkvPostArgs& a, hipStream_t stream);
 
 // PixelUnshuffle + flatten of latent frames into embedding operands [B F L, K_pad].
 hipError_t unshuffle_latent(const void* z, int z_kind, int B, int C, int F, int H, int W, int p,

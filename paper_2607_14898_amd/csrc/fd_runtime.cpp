@@ -335,46 +335,57 @@ fd_status run_stack(Ctx& x, const std::vector<LayerW>& layers, float* xs, int ro
   const int D = c.dim, H = c.mlp_hidden;
   const int n_units = rows_per_batch / U;
   const int64_t u0 = kc->t / c.unit_frames;
+  // geometry of the QKV post step (KV-norm, 3D-RoPE, ring append), shared by the layers
+  fd::QkvPostArgs qa;
+  qa.raw = kc->raw;
+  qa.q = kc->q;
+  qa.rope_axis = dec->rope_axis;
+  qa.rope_freq = dec->rope_freq;
+  qa.rope_hw = dec->rope_hw;
+  qa.rope_t = kc->rope_t;
+  qa.rope = c.rope;
+  qa.eps = c.norm_eps;
+  qa.B = B;
+  qa.N = c.n_heads;
+  qa.G = c.n_kv_groups;
+  qa.Dh = d.Dh;
+  qa.rows_per_batch = rows_per_batch;
+  qa.L = d.L;
+  qa.grid_w = d.grid_w;
+  qa.U = U;
+  qa.U_pad = U_pad;
+  qa.S = kc->S;
+  qa.u0 = u0;
+  qa.tau0 = tau0;
+  qa.out_kind = d.act_kind;
+  // temporal RoPE angles of this call's (sub-)frames, once for the whole stack
+  hipError_t e = fd::rope_time(qa, x.s);
+  if (e != hipSuccess) return fail(FD_ERR_DEVICE, "rope_time launch failed: %s", hipGetErrorString(e));
   for (size_t l = 0; l < layers.size(); ++l) {
     const LayerW& w = layers[l];
     fd_status st = run_norm(x, xs, rows, w.n1g, w.n1b);
     if (st) return st;
-    fd::GemmArgs g = gemm_args(kc->a, D, w.wqkv, rows, d.qkv_w, D, fd::EPI_STORE_F32, w.bqkv);
-    g.ep.out_f = kc->raw;
-    g.ep.ld_out = d.qkv_w;
-    if ((st = run_gemm(x, g, D))) return st;
-
-    fd::QkvPostArgs qa;
-    qa.raw = kc->raw;
-    qa.q = kc->q;
     qa.k_ring = kr[l];
     qa.vt_ring = vr[l];
     qa.knorm_g = c.kv_norm ? w.kg : nullptr;
     qa.vnorm_g = c.kv_norm ? w.vg : nullptr;
-    qa.rope_axis = dec->rope_axis;
-    qa.rope_freq = dec->rope_freq;
-    qa.rope_hw = dec->rope_hw;
-    qa.rope_t = kc->rope_t;
-    qa.rope = c.rope;
-    qa.eps = c.norm_eps;
-    qa.B = B;
-    qa.N = c.n_heads;
-    qa.G = c.n_kv_groups;
-    qa.Dh = d.Dh;
-    qa.rows_per_batch = rows_per_batch;
-    qa.L = d.L;
-    qa.grid_w = d.grid_w;
-    qa.U = U;
-    qa.U_pad = U_pad;
-    qa.S = kc->S;
-    qa.u0 = u0;
-    qa.tau0 = tau0;
-    qa.out_kind = d.act_kind;
     hipEvent_t ev;
-    if ((st = probe_begin(kc, FD_KC_QKV_POST, x.s, &ev))) return st;
-    hipError_t e = fd::qkv_post(qa, x.s);
-    if (e != hipSuccess) return fail(FD_ERR_DEVICE, "qkv_post launch failed: %s", hipGetErrorString(e));
-    if ((st = probe_end(kc, x.s, ev, (double)rows * d.qkv_w * (4.0 + d.act_bytes)))) return st;
+    fd::GemmArgs g;
+    if (d.is16) {
+      // 16-bit path: the post step runs in the projection's epilogue
+      g = gemm_args(kc->a, D, w.wqkv, rows, d.qkv_w, D, fd::EPI_QKV, w.bqkv);
+      g.ep.qkv = qa;
+      if ((st = run_gemm(x, g, D))) return st;
+    } else {
+      g = gemm_args(kc->a, D, w.wqkv, rows, d.qkv_w, D, fd::EPI_STORE_F32, w.bqkv);
+      g.ep.out_f = kc->raw;
+      g.ep.ld_out = d.qkv_w;
+      if ((st = run_gemm(x, g, D))) return st;
+      if ((st = probe_begin(kc, FD_KC_QKV_POST, x.s, &ev))) return st;
+      e = fd::qkv_post(qa, x.s);
+      if (e != hipSuccess) return fail(FD_ERR_DEVICE, "qkv_post launch failed: %s", hipGetErrorString(e));
+      if ((st = probe_end(kc, x.s, ev, (double)rows * d.qkv_w * (4.0 + d.act_bytes)))) return st;
+    }
 
     fd::AttnArgs aa;
     aa.q = kc->q;

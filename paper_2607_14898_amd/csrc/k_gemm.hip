@@ -158,10 +158,118 @@ __device__ __forceinline__ void tile_of(int bid, int n_tiles, int tiles_m, int t
 // before any of its stores: interleaved, every load would wait for the store
 // before it (the compiler cannot tell the addresses apart) and each element
 // would cost a full memory round trip.
+// x / d for 0 <= x < 2^23 and 0 < d, given inv = 1.0f / d (float product, then
+// one exact integer correction)
+__device__ __forceinline__ int div_small(int x, int d, float inv) {
+  int q = (int)((float)x * inv);
+  const int r = x - q * d;
+  return q + (r >= d) - (r < 0);
+}
+
 template <int EPI, typename T, int FM, int FN>
 __device__ __forceinline__ void store_tile(const EpiParams& ep, const f32x16 (&acc)[FM][FN], int r0,
-                                           int c0, int M, int N, int lr, int lk) {
-  if constexpr (EPI == EPI_SWIGLU) {
+                                           int c0, int M, int N, int lr, int lk, float* ws) {
+  if constexpr (EPI == EPI_QKV) {
+    // The QKV projection's post step (Sec. 3.2, Eq. kv_cache): a wave's 64
+    // columns are one head vector (head slot c0 / 64: query heads, then key
+    // groups, then value groups). Each 32-row block of the wave goes through
+    // the wave's share of the stage buffers (free once the K loop is done): 16 lanes then hold
+    // 4 columns of one row, so the KV-norm (RMS over the 64 columns) is a
+    // 16-lane sum and the 3D-RoPE pairs sit inside a lane. Queries go to the
+    // query buffer, keys to their ring slot, values (normalised in LDS, then
+    // one lane per column) transposed to the V ring.
+    static_assert(FN == 2, "one 64-column head vector per wave");
+    const QkvPostArgs& a = ep.qkv;
+    const int lane = lk * 32 + lr;
+    const int wave = threadIdx.x >> 6;
+    const int hs = c0 >> 6;
+    const bool is_q = hs < a.N, is_v = hs >= a.N + a.G;
+    const float* gn = is_q ? nullptr : (is_v ? a.vnorm_g : a.knorm_g);
+    const int kvg = hs - a.N - (is_v ? a.G : 0);  // KV group
+    const int cq = 4 * (lane & 15);               // this lane's 4 columns in the second pass
+    float4 gq = make_float4(1.f, 1.f, 1.f, 1.f);
+    if (gn) gq = *reinterpret_cast<const float4*>(gn + cq);
+    const bool rope = a.rope && !is_v;
+    const int pa = cq >> 1;  // RoPE pairs pa and pa + 1 of columns cq .. cq + 3
+    const int ax0 = rope ? a.rope_axis[pa] : 0, ax1 = rope ? a.rope_axis[pa + 1] : 0;
+    const float inv_rpb = 1.f / a.rows_per_batch, inv_L = 1.f / a.L;
+    const float inv_gw = 1.f / a.grid_w, inv_U = 1.f / a.U;
+    const int slot0 = (int)(a.u0 % a.S);
+    const float bias0 = ep.bias[min(c0, N - 64) + lr], bias1 = ep.bias[min(c0, N - 64) + 32 + lr];
+    constexpr int LS = 68;  // row stride: rows 4 apart fall in other banks, rows stay 16-byte aligned
+    float* wl = ws + wave * (32 * LS);  // [32 rows][64 columns]
+    // row of the call -> (stream, unit, position) and (sub-frame, h, w)
+    auto split = [&](int row, int& b, int& lu, int& pos, int& fs, int& hh, int& ww) {
+      b = div_small(row, a.rows_per_batch, inv_rpb);
+      const int rb = row - b * a.rows_per_batch;
+      lu = div_small(rb, a.U, inv_U);
+      pos = rb - lu * a.U;
+      fs = div_small(rb, a.L, inv_L);
+      const int tok = rb - fs * a.L;
+      hh = div_small(tok, a.grid_w, inv_gw);
+      ww = tok - hh * a.grid_w;
+    };
+    __syncthreads();  // every wave is past its last read of the stage buffers
+    if (c0 >= N) return;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int rbase = r0 + i * 32;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rr = 8 * (r >> 2) + 4 * lk + (r & 3);
+        wl[rr * LS + lr] = acc[i][0][r] + bias0;
+        wl[rr * LS + 32 + lr] = acc[i][1][r] + bias1;
+      }
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's LDS writes are done
+      for (int it = 0; it < 8; ++it) {
+        const int rr = it * 4 + (lane >> 4);
+        const int row_t = rbase + rr, row = min(row_t, M - 1);
+        float4 v = *reinterpret_cast<const float4*>(wl + rr * LS + cq);
+        if (gn) {
+          float ss = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+#pragma unroll
+          for (int o = 1; o < 16; o <<= 1) ss += __shfl_xor(ss, o);
+          const float rn = rsqrtf(ss * (1.f / 64.f) + a.eps);
+          v = make_float4(v.x * rn * gq.x, v.y * rn * gq.y, v.z * rn * gq.z, v.w * rn * gq.w);
+        }
+        int b, lu, pos, fs, hh, ww;
+        split(row, b, lu, pos, fs, hh, ww);
+        if (rope) {
+          const float2 c0v = ax0 == 0 ? a.rope_t[fs * 32 + pa] : a.rope_hw[(ax0 == 1 ? hh : ww) * 32 + pa];
+          const float2 c1v = ax1 == 0 ? a.rope_t[fs * 32 + pa + 1] : a.rope_hw[(ax1 == 1 ? hh : ww) * 32 + pa + 1];
+          v = make_float4(v.x * c0v.x - v.y * c0v.y, v.x * c0v.y + v.y * c0v.x,
+                          v.z * c1v.x - v.w * c1v.y, v.z * c1v.y + v.w * c1v.x);
+        }
+        if (is_v) {  // normalised values back to LDS for the transposed store
+          *reinterpret_cast<float4*>(wl + rr * LS + cq) = v;
+          continue;
+        }
+        if (row_t >= M) continue;
+        T o4[4] = {to_act<T>(v.x), to_act<T>(v.y), to_act<T>(v.z), to_act<T>(v.w)};
+        T* dst;
+        if (is_q) {
+          dst = (T*)a.q + (int64_t)row * (a.N * 64) + c0 + cq;
+        } else {
+          const int slot = (slot0 + lu) % a.S;
+          dst = (T*)a.k_ring + (((int64_t)(b * a.G + kvg) * a.S + slot) * a.U_pad + pos) * 64 + cq;
+        }
+        *reinterpret_cast<uint2*>(dst) = *reinterpret_cast<const uint2*>(o4);
+      }
+      if (is_v) {  // lane = column (dimension): V^T[dim][pos] for the block's rows
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+        for (int rr = 0; rr < 32; ++rr) {
+          const int row_t = rbase + rr;
+          if (row_t >= M) break;
+          int b, lu, pos, fs, hh, ww;
+          split(row_t, b, lu, pos, fs, hh, ww);
+          const int slot = (slot0 + lu) % a.S;
+          T* vt = (T*)a.vt_ring + ((int64_t)(b * a.G + kvg) * a.S + slot) * 64 * a.U_pad + pos;
+          vt[(int64_t)lane * a.U_pad] = to_act<T>(wl[rr * LS + lane]);
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // the block's LDS reads are done before the next block
+    }
+  } else if constexpr (EPI == EPI_SWIGLU) {
     float bg[FN / 2], bu[FN / 2];
 #pragma unroll
     for (int j = 0; j < FN; j += 2) {
@@ -393,7 +501,8 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
     sc = sn;
   }
   mfmas(1);
-  store_tile<EPI, T, FM, FN>(ep, acc, m0 + wm0, n0 + wn0, M, N, lr, lk);
+  static_assert(EPI != EPI_QKV || NW * 32 * 68 * 4 <= NS * STAGE * 16, "QKV epilogue staging fits the stage buffers");
+  store_tile<EPI, T, FM, FN>(ep, acc, m0 + wm0, n0 + wn0, M, N, lr, lk, reinterpret_cast<float*>(lds));
 }
 
 template <typename T, class C, int EPI>
@@ -443,6 +552,7 @@ hipError_t dispatch_epi(const GemmArgs& g, hipStream_t s) {
     case EPI_TUP: return dispatch_tiles<T, EPI_TUP>(g, s);
     case EPI_PIXEL: return dispatch_tiles<T, EPI_PIXEL>(g, s);
     case EPI_LINEAR_PIXEL: return dispatch_tiles<T, EPI_LINEAR_PIXEL>(g, s);
+    case EPI_QKV: return dispatch_tiles<T, EPI_QKV>(g, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -508,7 +618,8 @@ hipError_t launch_f32(const GemmArgs& g, hipStream_t s) {
 hipError_t gemm_mfma(Act16 t, const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
   if (g.K <= 0 || g.K % BKD || g.lda % 8 || g.ldw != g.K) return hipErrorInvalidValue;
-  if (g.epi == EPI_SWIGLU && g.N % 64) return hipErrorInvalidValue;
+  if ((g.epi == EPI_SWIGLU || g.epi == EPI_QKV) && g.N % 64) return hipErrorInvalidValue;
+  if (g.epi == EPI_QKV && g.ep.qkv.Dh != 64) return hipErrorInvalidValue;
   return t == Act16::F16 ? dispatch_epi<_Float16>(g, s) : dispatch_epi<__hip_bfloat16>(g, s);
 }
 

@@ -272,15 +272,18 @@ hipError_t norm_rows(const float* x, int M, int D, const float* g, const float* 
   return hipGetLastError();
 }
 
+hipError_t rope_time(const QkvPostArgs& a, hipStream_t s) {
+  if (!a.rope || a.rows_per_batch <= 0) return hipSuccess;
+  const int n_fs = a.rows_per_batch / a.L, np = a.Dh / 2;
+  hipLaunchKernelGGL(rope_time_kernel, dim3((n_fs * np + 255) / 256), dim3(256), 0, s, a.tau0,
+                     n_fs, np, a.rope_axis, a.rope_freq, a.rope_t);
+  return hipGetLastError();
+}
+
 hipError_t qkv_post(const QkvPostArgs& a, hipStream_t s) {
   const int rows = a.B * a.rows_per_batch;
   if (rows <= 0) return hipSuccess;
   if (a.Dh > 64 || a.Dh % 8 || a.rows_per_batch % a.U) return hipErrorInvalidValue;
-  if (a.rope) {
-    const int n_fs = a.rows_per_batch / a.L, np = a.Dh / 2;
-    hipLaunchKernelGGL(rope_time_kernel, dim3((n_fs * np + 255) / 256), dim3(256), 0, s, a.tau0,
-                       n_fs, np, a.rope_axis, a.rope_freq, a.rope_t);
-  }
   const int64_t threads = (int64_t)rows * (a.N + a.G) * (a.Dh / 4);
   hipLaunchKernelGGL(qk_post_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, a, rows);
   const int blocks_per_unit = (a.U + VP_ROWS - 1) / VP_ROWS;

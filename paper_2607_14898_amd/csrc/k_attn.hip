@@ -11,7 +11,7 @@
 // wave owns 64 queries as two 32-query MFMA blocks and computes S^T = K Q^T
 // with the 32x32x16 MFMA, so a lane holds one query and 16 key scores per 32-key
 // block: the softmax max needs one cross-half exchange per tile and the row
-// sums stay lane-local (v_dot2 over the f16 probabilities) until the end. K
+// sums stay lane-local (fp32 adds of the probabilities) until the end. K
 // rows are fed to the MFMA in the order that makes the score registers of a
 // lane exactly the B operand of the following O^T += V^T P^T MFMA, so P never
 // leaves registers. Queries are pre-scaled by log2(e) / sqrt(D_h), and one
@@ -39,15 +39,6 @@ template <> struct AMfma<_Float16> {
     return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
   }
   static __device__ __forceinline__ E cvt(float x) { return (_Float16)x; }
-  // sum of the 8 values of an operand, accumulated in fp32 (v_dot2_f32_f16)
-  static __device__ __forceinline__ float sum8(const V& p) {
-    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
-    const h2 one = {(_Float16)1.f, (_Float16)1.f};
-    float acc = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; i += 2) acc = __builtin_amdgcn_fdot2((h2){p[i], p[i + 1]}, one, acc, false);
-    return acc;
-  }
 };
 template <> struct AMfma<__hip_bfloat16> {
   using V = bf16x8;
@@ -56,12 +47,6 @@ template <> struct AMfma<__hip_bfloat16> {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   }
   static __device__ __forceinline__ E cvt(float x) { return (__bf16)x; }
-  static __device__ __forceinline__ float sum8(const V& p) {
-    float acc = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) acc += (float)p[i];
-    return acc;
-  }
 };
 
 // LDS chunk position inside a [64 rows][8 x 16-byte chunks] tile. gfx950 LDS
@@ -265,17 +250,25 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
     auto exp_tile = [&]() {
 #pragma unroll
       for (int qb = 0; qb < NQB; ++qb) {
-        float sum = 0.f;
+        // row sum of the fp32 probabilities by a pairwise tree (plain adds
+        // overlap the MFMAs; the packed-f16 dot instruction does not)
+        float t[32];
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int h = 0; h < 2; ++h) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-              pf[qb][kb * 2 + h][e] = M::cvt(__builtin_amdgcn_exp2f(s[kb][qb][8 * h + e]));
-            sum += M::sum8(pf[qb][kb * 2 + h]);
+            for (int e = 0; e < 8; ++e) {
+              const float p = __builtin_amdgcn_exp2f(s[kb][qb][8 * h + e]);
+              pf[qb][kb * 2 + h][e] = M::cvt(p);
+              t[(kb * 2 + h) * 8 + e] = p;
+            }
           }
-        ls[qb] = sum;
+#pragma unroll
+        for (int w = 16; w >= 1; w >>= 1)
+#pragma unroll
+          for (int i = 0; i < w; ++i) t[i] = t[i] + t[i + w];
+        ls[qb] = t[0];
       }
     };
     scores();

@@ -14,12 +14,12 @@
 // sums stay lane-local (fp32 adds of the probabilities) until the end. K
 // rows are fed to the MFMA in the order that makes the score registers of a
 // lane exactly the B operand of the following O^T += V^T P^T MFMA, so P never
-// leaves registers. Queries are pre-scaled by log2(e) / sqrt(D_h), and one
-// extra MFMA k-step subtracts each query's running shift, so the MFMA output
-// is the exp2 argument itself. The shift is raised (and O and the row sum
-// rescaled) only on the first tile and when some probability of a lane could
-// leave the f16 range; only the ragged last tile of a unit is masked. K and
-// V^T tiles of 64 keys are double-buffered in LDS.
+// leaves registers. Queries are pre-scaled by log2(e) / sqrt(D_h), and each
+// score accumulator starts from the query's negated running shift (the MFMA's
+// C operand), so the MFMA output is the exp2 argument itself. The shift is
+// raised (and O and the row sum rescaled) only on the first tile and when some
+// probability of a lane could leave the f16 range; only the ragged last tile
+// of a unit is masked. K and V^T tiles of 64 keys are double-buffered in LDS.
 #include "fd_kernels.h"
 
 #include <hip/hip_bf16.h>
@@ -173,22 +173,18 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
     asm volatile("" ::: "memory");
   };
 
-  // Running shift m_q of each query, kept as an f16 value: an extra 16-wide
-  // k-step multiplies the constant columns (1, mask, 0, ..., 0) of K with
-  // (-m_q, 1, 0, ...) of Q, so the MFMA returns c q.k - m_q (and -60000 more
-  // for the padding keys of a ragged tile) and P = exp2(S^T) needs no VALU
-  // work before the exponential. The shift only has to keep P in f16
-  // range: it is raised (and O, l rescaled by the exact exp2 of the change of
-  // the f16 shifts) on the first tile and whenever some p of a lane may exceed
+  // Running shift m_q of each query, kept as an f16-representable value. The
+  // score MFMAs accumulate onto cinit = -m_q, so they return c q.k - m_q and
+  // P = exp2(S^T) needs no VALU work before the exponential. The shift only has
+  // to keep P in f16 range: it is raised (and O, l rescaled by the exact exp2
+  // of the change) on the first tile and whenever some p of a lane may exceed
   // 2^15, detected from the lane's partial row sum of the tile.
-  V kone, mqf[NQB];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    kone[e] = M::cvt(e == 0 && lh == 0 ? 1.f : 0.f);
-#pragma unroll
-    for (int qb = 0; qb < NQB; ++qb) mqf[qb][e] = M::cvt(e == 1 && lh == 0 ? 1.f : 0.f);
-  }
   float mq[NQB], l_run[NQB];
+  f32x16 cinit[NQB];
+#pragma unroll
+  for (int qb = 0; qb < NQB; ++qb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) cinit[qb][r] = 0.f;
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb) mq[qb] = l_run[qb] = 0.f;
   f32x16 acc[NQB][2];
@@ -226,23 +222,26 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
         }
       __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        // second column of the constant K operand: -60000 on the padding keys
-        // of a unit's ragged last tile, so exp2 of their scores is 0
-        V ka = kone;
-        ka[1] = M::cvt(tail && lh == 0 && kb * 32 + key_of_row(lr) >= tail_valid ? -60000.f : 0.f);
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int qb = 0; qb < NQB; ++qb) s[kb][qb] = M::run(ka, mqf[qb], f32x16{});
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
+        for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
           for (int qb = 0; qb < NQB; ++qb) {
             const uint4 w = sq[wave][(qb * 4 + ks) * 64 + lane];
-            s[kb][qb] = M::run(kfr[kb][ks], *reinterpret_cast<const V*>(&w), s[kb][qb]);
+            s[kb][qb] = M::run(kfr[kb][ks], *reinterpret_cast<const V*>(&w), ks == 0 ? cinit[qb] : s[kb][qb]);
           }
-        }
-      }
       __builtin_amdgcn_s_setprio(0);
+      // the padding keys of a unit's ragged last tile: register r of a lane
+      // holds key 16 (r / 8) + 8 lh + r % 8 of its 32-key block
+      if (tail) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int qb = 0; qb < NQB; ++qb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              if (kb * 32 + 16 * (r >> 3) + 8 * lh + (r & 7) >= tail_valid) s[kb][qb][r] = -INFINITY;
+      }
     };
     // P = exp2(S^T) in f16, laid out as the B operand of O^T += V^T P^T
     V pf[NQB][4];
@@ -293,7 +292,8 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
         const float mq_new = (float)M::cvt(mq[qb] + fmaxf(m0, 0.f));
         const float delta = mq_new - mq[qb];  // exact: both are f16 values
         mq[qb] = mq_new;
-        mqf[qb][0] = M::cvt(lh == 0 ? -mq_new : 0.f);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) cinit[qb][r] = -mq_new;
         const float alpha = __builtin_amdgcn_exp2f(-delta);
         l_run[qb] *= alpha;
 #pragma unroll

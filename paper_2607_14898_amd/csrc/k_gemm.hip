@@ -26,7 +26,9 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-__device__ __forceinline__ float silu_f(float x) { return x / (1.f + __expf(-x)); }
+// SiLU with the hardware reciprocal (1 ulp) instead of an IEEE division; the
+// limits hold: x -> -inf gives x * rcp(inf) = -0.
+__device__ __forceinline__ float silu_f(float x) { return x * __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
 __device__ __forceinline__ float gelu_f(float x) { return 0.5f * x * (1.f + erff(x * 0.70710678118654752f)); }
 
 template <typename T> __device__ __forceinline__ T to_act(float v);
@@ -166,7 +168,7 @@ __device__ __forceinline__ int div_small(int x, int d, float inv) {
   return q + (r >= d) - (r < 0);
 }
 
-template <int EPI, typename T, int FM, int FN>
+template <int EPI, typename T, int FM, int FN, bool FAST_RMW>
 __device__ __forceinline__ void store_tile(const EpiParams& ep, const f32x16 (&acc)[FM][FN], int r0,
                                            int c0, int M, int N, int lr, int lk, float* ws) {
   if constexpr (EPI == EPI_QKV) {
@@ -303,6 +305,11 @@ __device__ __forceinline__ void store_tile(const EpiParams& ep, const f32x16 (&a
       cb[j] = ep.bias[col];
       cok[j] = c0 + j * 32 + lr < N;
     }
+    // interior blocks (the wave's rows and columns all in range) skip the
+    // per-element checks; for the residual read-modify-write only where other
+    // waves of the CU cover its load latency (measured: slower on a lone
+    // 4-wave workgroup per CU)
+    const bool interior = (EPI != EPI_RESID_ADD || FAST_RMW) && r0 + FM * 32 <= M && c0 + FN * 32 <= N;
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
       int64_t ro[16];
@@ -312,6 +319,38 @@ __device__ __forceinline__ void store_tile(const EpiParams& ep, const f32x16 (&a
         const int row = r0 + i * 32 + 8 * (r >> 2) + 4 * lk + (r & 3);
         rok[r] = row < M;
         ro[r] = row_off<EPI>(ep, min(row, M - 1));
+      }
+      if (interior) {
+        if constexpr (EPI == EPI_RESID_ADD || EPI == EPI_STORE_F32) {
+          // row-major destination: column blocks j are 32 floats apart, an
+          // immediate offset from one row pointer
+          float* rp[16];
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            rp[r] = ep.out_f + (int64_t)(r0 + i * 32 + 8 * (r >> 2) + 4 * lk + (r & 3)) * ep.ld_out + c0 + lr;
+          if constexpr (EPI == EPI_RESID_ADD) {
+            float old[16][FN];
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+#pragma unroll
+              for (int j = 0; j < FN; ++j) old[r][j] = rp[r][32 * j];
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+#pragma unroll
+              for (int j = 0; j < FN; ++j) rp[r][32 * j] = old[r][j] + (acc[i][j][r] + cb[j]);
+          } else {
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+#pragma unroll
+              for (int j = 0; j < FN; ++j) rp[r][32 * j] = acc[i][j][r] + cb[j];
+          }
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) epi_store<EPI, T>(ep, ro[r] + coff[j], acc[i][j][r] + cb[j]);
+        }
+        continue;
       }
       if constexpr (EPI == EPI_RESID_ADD) {
         float old[16][FN];
@@ -330,6 +369,128 @@ __device__ __forceinline__ void store_tile(const EpiParams& ep, const f32x16 (&a
 #pragma unroll
           for (int j = 0; j < FN; ++j)
             if (rok[r] && cok[j]) epi_store<EPI, T>(ep, ro[r] + coff[j], acc[i][j][r] + cb[j]);
+      }
+    }
+  }
+}
+
+// Epilogue of one wave's blocks computed transposed (acc[i][j] = W block j
+// times A block i): lane (lk, lr) holds output row r0 + 32 i + lr and, in
+// registers 4 q .. 4 q + 3, the four consecutive columns c0 + 32 j + 8 q +
+// 4 lk + 0..3. Every destination access covers those four columns at once (one
+// 16-byte fp32 or 8-byte 16-bit access) whenever the four land contiguously;
+// vec == false (a ragged or unaligned destination) stores element by element.
+template <int EPI, typename T, int FM, int FN>
+__device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (&acc)[FM][FN], int r0,
+                                             int c0, int M, int N, int lr, int lk, bool vec) {
+  typedef __attribute__((ext_vector_type(4))) float f4;
+  int64_t ro[FM];
+  bool rok[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int row = r0 + i * 32 + lr;
+    rok[i] = row < M;
+    ro[i] = row_off<EPI>(ep, min(row, M - 1));
+  }
+  if constexpr (EPI == EPI_SWIGLU) {
+    // gate block j and up block j + 1 give output columns (c0 + 32 j) / 2 + 0..31
+#pragma unroll
+    for (int j = 0; j < FN; j += 2)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int lc = 8 * q + 4 * lk, pc = c0 + j * 32 + lc;
+        if (pc >= N) continue;  // N % 64 == 0: a group is valid as a whole
+        float bg[4], bu[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          bg[e] = ep.bias[pc + e];
+          bu[e] = ep.bias[pc + 32 + e];
+        }
+        const int oc = (c0 + j * 32) / 2 + lc;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+          if (!rok[i]) continue;
+          T o4[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            o4[e] = to_act<T>(silu_f(acc[i][j][4 * q + e] + bg[e]) * (acc[i][j + 1][4 * q + e] + bu[e]));
+          *reinterpret_cast<uint2*>((T*)ep.out_a + ro[i] + oc) = *reinterpret_cast<const uint2*>(o4);
+        }
+      }
+  } else {
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      int64_t co[4];
+      float cb[4][4];
+      bool cok[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int n = c0 + j * 32 + 8 * q + 4 * lk;
+        cok[q] = n < N;
+        co[q] = col_off<EPI>(ep, min(n, N - 1));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) cb[q][e] = ep.bias[min(n + e, N - 1)];
+      }
+      if (!vec) {  // element by element
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int n = c0 + j * 32 + 8 * q + 4 * lk + e;
+              if (rok[i] && n < N)
+                epi_store<EPI, T>(ep, ro[i] + col_off<EPI>(ep, n), acc[i][j][4 * q + e] + cb[q][e]);
+            }
+        continue;
+      }
+      if constexpr (EPI == EPI_RESID_ADD) {
+        // the four loads of a row before its stores (the compiler cannot tell
+        // the addresses apart and would otherwise serialise each pair)
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+          if (!rok[i]) continue;
+          f4 old[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (cok[q]) old[q] = *reinterpret_cast<const f4*>(ep.out_f + ro[i] + co[q]);
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (cok[q]) {
+              f4 v;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = old[q][e] + (acc[i][j][4 * q + e] + cb[q][e]);
+              *reinterpret_cast<f4*>(ep.out_f + ro[i] + co[q]) = v;
+            }
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            if (!(rok[i] && cok[q])) continue;
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e] + cb[q][e];
+            const int64_t off = ro[i] + co[q];
+            if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_TUP) {
+              *reinterpret_cast<f4*>(ep.out_f + off) = f4{v[0], v[1], v[2], v[3]};
+            } else if constexpr (EPI == EPI_PIXEL || EPI == EPI_LINEAR_PIXEL) {
+              if (ep.clamp)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = fminf(1.f, fmaxf(-1.f, v[e]));
+              *reinterpret_cast<f4*>(ep.out_f + off) = f4{v[0], v[1], v[2], v[3]};
+            } else {
+              T o4[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                if constexpr (EPI == EPI_STORE_SILU) o4[e] = to_act<T>(silu_f(v[e]));
+                else if constexpr (EPI == EPI_STORE_GELU) o4[e] = to_act<T>(gelu_f(v[e]));
+                else o4[e] = to_act<T>(v[e]);
+              }
+              *reinterpret_cast<uint2*>((T*)ep.out_a + off) = *reinterpret_cast<const uint2*>(o4);
+            }
+          }
       }
     }
   }
@@ -374,10 +535,17 @@ struct TileCfg {
 // so the compiler neither sees nor orders them; every ordering they need is
 // explicit: s_waitcnt on the wave's own DMAs, then s_barrier (with compiler
 // memory barriers around it) before any wave reads the tile or refills a stage.
+// Epilogues with 16-bit destinations take the accumulators transposed: four
+// consecutive columns per lane make one 8-byte store and one bias / SiLU pass
+// per four values. fp32 destinations keep the direct layout, where the 32 lanes
+// of a half-wave write one full 128-byte row segment per store.
+template <int EPI> constexpr bool kTransposed =
+    EPI == EPI_SWIGLU || EPI == EPI_STORE_ACT || EPI == EPI_STORE_SILU || EPI == EPI_STORE_GELU;
+
 template <typename T, class C, int EPI>
 __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
     const T* __restrict__ A, const T* __restrict__ W, int M, int N, int K, int lda, int ldw,
-    EpiParams ep, int tiles_m, int tiles_n) {
+    EpiParams ep, int tiles_m, int tiles_n, int vec_store) {
   constexpr int BM = C::BM, BN = C::BN, FM = C::FM, FN = C::FN, NS = C::NS, NW = C::NW;
   constexpr int QA = C::QA, Q = C::QA + C::QB, STAGE = C::STAGE;
   using V = typename Mfma<T>::V;
@@ -472,7 +640,9 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::run(fa[slot][i], fb[slot][j], acc[i][j]);
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = kTransposed<EPI> ? Mfma<T>::run(fb[slot][j], fa[slot][i], acc[i][j])
+                                     : Mfma<T>::run(fa[slot][i], fb[slot][j], acc[i][j]);
   };
 
   // Tile t sits in stage t % NS. The loop starts at the barrier (whose
@@ -502,14 +672,24 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
   }
   mfmas(1);
   static_assert(EPI != EPI_QKV || NW * 32 * 68 * 4 <= NS * STAGE * 16, "QKV epilogue staging fits the stage buffers");
-  store_tile<EPI, T, FM, FN>(ep, acc, m0 + wm0, n0 + wn0, M, N, lr, lk, reinterpret_cast<float*>(lds));
+  if constexpr (kTransposed<EPI>)
+    store_tile_t<EPI, T, FM, FN>(ep, acc, m0 + wm0, n0 + wn0, M, N, lr, lk, vec_store != 0);
+  else
+    store_tile<EPI, T, FM, FN, !(C::NW == 4 && C::MIN_BLOCKS == 1)>(ep, acc, m0 + wm0, n0 + wn0, M, N, lr, lk,
+                                                                   reinterpret_cast<float*>(lds));
 }
 
 template <typename T, class C, int EPI>
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   const int tm = (g.M + C::BM - 1) / C::BM, tn = (g.N + C::BN - 1) / C::BN;
+  // four consecutive output columns land contiguously and 16-byte aligned
+  // (fp32) / 8-byte aligned (16-bit) in the destination
+  bool vec = g.N % 4 == 0 && g.ep.ld_out % 4 == 0;
+  if (EPI == EPI_PIXEL || EPI == EPI_LINEAR_PIXEL) vec = vec && g.ep.s % 4 == 0;
+  if (EPI == EPI_TUP) vec = vec && g.ep.dim % 4 == 0;
+  vec = vec && ((uintptr_t)g.ep.out_f % 16 == 0) && ((uintptr_t)g.ep.out_a % 8 == 0);
   hipLaunchKernelGGL((gemm_mfma_kernel<T, C, EPI>), dim3(tm * tn), dim3(C::NT), 0, s,
-                     (const T*)g.A, (const T*)g.W, g.M, g.N, g.K, g.lda, g.ldw, g.ep, tm, tn);
+                     (const T*)g.A, (const T*)g.W, g.M, g.N, g.K, g.lda, g.ldw, g.ep, tm, tn, vec ? 1 : 0);
   return hipGetLastError();
 }
 

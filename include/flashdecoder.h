@@ -186,6 +186,18 @@ fd_status fd_probe_enable(fd_kv_cache* cache, int32_t kernel_class);
 fd_status fd_probe_read(fd_kv_cache* cache, double* total_ms, int64_t* launches,
                         double* work);
 
+/* Sustained dense MFMA throughput of the current device (a measurement aid
+ * beside the datasheet peak, which assumes the peak engine clock). Runs two
+ * 4-wave workgroups per compute unit, each wave issuing `iters` x 16
+ * back-to-back 32x32x16 MFMAs (dtype FD_DTYPE_F16 or FD_DTYPE_BF16) on
+ * operands that change every instruction, three launches back to back on
+ * `stream` (NULL = default), and times the last with HIP events. Writes the
+ * achieved TFLOP/s and the mean shader clock (GHz) of that launch. Blocks until
+ * done; allocates and frees its own small device buffers. iters in [1, 10^7],
+ * else INVALID_ARGUMENT; HIP failures give DEVICE. */
+fd_status fd_measure_mfma_peak(int32_t dtype, int32_t iters, void* stream, double* tflops,
+                               double* clock_ghz);
+
 const char* fd_status_string(fd_status status);
 
 /* Message of the last failed call on this thread ("" if none). */

@@ -11,7 +11,8 @@ from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SOURCES = ["csrc/k_gemm.hip", "csrc/k_attn.hip", "csrc/k_misc.hip", "csrc/fd_runtime.cpp"]
+SOURCES = ["csrc/k_gemm.hip", "csrc/k_attn.hip", "csrc/k_misc.hip", "csrc/k_probe.hip",
+           "csrc/fd_runtime.cpp"]
 LIB = os.path.join(PKG, "libflashdecoder.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",

@@ -122,6 +122,13 @@ hipError_t unshuffle_latent(const void* z, int z_kind, int B, int C, int F, int 
 // h[m, j] = SiLU(raw[m, j]) * raw[m, H + j]  (fp32 path, un-interleaved weights)
 hipError_t swiglu_f32(const float* raw, int M, int H, float* h, hipStream_t stream);
 
+// Sustained MFMA throughput probe: `blocks` workgroups of 4 waves issue 16
+// 32x32x16 MFMAs per iteration each; clk receives per workgroup the shader
+// cycles and wall-clock ticks of its loop ([blocks][2]), sink blocks * 256
+// floats.
+hipError_t mfma_peak(Act16 t, int blocks, int iters, unsigned long long* clk, float* sink,
+                     hipStream_t stream);
+
 // Convert a host-prepared fp32 array on the device into 16-bit operands.
 hipError_t convert_f32_to_16(const float* src, void* dst, int64_t n, int out_kind,
                              hipStream_t stream);

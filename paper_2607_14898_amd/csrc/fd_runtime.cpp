@@ -977,6 +977,65 @@ fd_status fd_probe_read(fd_kv_cache* cache, double* total_ms, int64_t* launches,
   return FD_OK;
 }
 
+fd_status fd_measure_mfma_peak(int32_t dtype, int32_t iters, void* stream, double* tflops,
+                               double* clock_ghz) {
+  if (!tflops || !clock_ghz) return fail(FD_ERR_INVALID_ARGUMENT, "output pointer is NULL");
+  if (dtype != FD_DTYPE_F16 && dtype != FD_DTYPE_BF16)
+    return fail(FD_ERR_INVALID_ARGUMENT, "dtype must be FD_DTYPE_F16 or FD_DTYPE_BF16");
+  if (iters < 1 || iters > 10000000) return fail(FD_ERR_INVALID_ARGUMENT, "iters out of range");
+  int dev = 0, cus = 0, wclk_khz = 0;
+  FD_HIP(hipGetDevice(&dev));
+  FD_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  FD_HIP(hipDeviceGetAttribute(&wclk_khz, hipDeviceAttributeWallClockRate, dev));
+  if (cus <= 0 || wclk_khz <= 0) return fail(FD_ERR_DEVICE, "device attributes unavailable");
+  const int blocks = 2 * cus;
+  hipStream_t s = (hipStream_t)stream;
+  unsigned long long* clk = nullptr;
+  float* sink = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  fd_status st = FD_OK;
+  std::vector<unsigned long long> h(2 * (size_t)blocks);
+  float ms = 0.f;
+  do {
+    if (hipMalloc(&clk, h.size() * sizeof(unsigned long long)) != hipSuccess ||
+        hipMalloc(&sink, (size_t)blocks * 256 * sizeof(float)) != hipSuccess) {
+      st = fail(FD_ERR_OUT_OF_MEMORY, "probe buffers");
+      break;
+    }
+    if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
+      st = fail(FD_ERR_DEVICE, "hipEventCreate failed");
+      break;
+    }
+    const fd::Act16 t = dtype == FD_DTYPE_F16 ? fd::Act16::F16 : fd::Act16::BF16;
+    hipError_t e = fd::mfma_peak(t, blocks, iters, clk, sink, s);
+    if (e == hipSuccess) e = fd::mfma_peak(t, blocks, iters, clk, sink, s);
+    if (e == hipSuccess) e = hipEventRecord(e0, s);
+    if (e == hipSuccess) e = fd::mfma_peak(t, blocks, iters, clk, sink, s);
+    if (e == hipSuccess) e = hipEventRecord(e1, s);
+    if (e == hipSuccess) e = hipEventSynchronize(e1);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+    if (e == hipSuccess)
+      e = hipMemcpy(h.data(), clk, h.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) {
+      st = fail(FD_ERR_DEVICE, "MFMA probe failed: %s", hipGetErrorString(e));
+      break;
+    }
+  } while (false);
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  if (clk) (void)hipFree(clk);
+  if (sink) (void)hipFree(sink);
+  if (st != FD_OK) return st;
+  double cyc = 0.0, ticks = 0.0;
+  for (int b = 0; b < blocks; ++b) {
+    cyc += (double)h[2 * b];
+    ticks += (double)h[2 * b + 1];
+  }
+  *tflops = (double)blocks * 4.0 * iters * 16.0 * 32768.0 / (ms * 1e-3) / 1e12;
+  *clock_ghz = ticks > 0 ? cyc / ticks * wclk_khz * 1e-6 : 0.0;
+  return FD_OK;
+}
+
 const char* fd_status_string(fd_status s) {
   switch (s) {
     case FD_OK: return "ok";

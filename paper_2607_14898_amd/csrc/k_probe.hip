@@ -1,0 +1,87 @@
+// Sustained dense MFMA throughput of the GPU this library runs on.
+//
+// The datasheet MFMA peak assumes the 2.4 GHz peak engine clock; under a dense
+// MFMA load the chip's power and current management lowers the clock, and the
+// throughput that load actually sustains is what the decoder's GEMMs and
+// attention are measured against beside the datasheet figure. Every wave of
+// two 4-wave workgroups per CU issues 32x32x16 MFMAs back to back on eight
+// accumulators, with operands that change every instruction (pseudo-random
+// values in [-1, 1), like real activations and weights), and records its
+// shader-clock cycles and wall-clock ticks.
+#include "fd_kernels.h"
+
+#include <hip/hip_bf16.h>
+
+namespace fd {
+namespace {
+
+typedef _Float16 h16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 b16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16p __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ float hash_unit(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x7feb352du;
+  x ^= x >> 15;
+  x *= 0x846ca68bu;
+  x ^= x >> 16;
+  return (float)(x & 0xFFFFu) * (1.f / 32768.f) - 1.f;
+}
+
+template <typename V, typename E>
+__device__ __forceinline__ f32x16p mfma_op(V a, V b, f32x16p c);
+template <>
+__device__ __forceinline__ f32x16p mfma_op<h16x8, _Float16>(h16x8 a, h16x8 b, f32x16p c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+template <>
+__device__ __forceinline__ f32x16p mfma_op<b16x8, __bf16>(b16x8 a, b16x8 b, f32x16p c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+template <typename V, typename E>
+__global__ __launch_bounds__(256) void mfma_peak_kernel(int iters, unsigned long long* clk, float* sink) {
+  const uint32_t gid = blockIdx.x * 256 + threadIdx.x;
+  V a[8], b[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      a[i][e] = (E)hash_unit(gid * 131u + i * 8u + e);
+      b[i][e] = (E)hash_unit(gid * 131u + 64u + i * 8u + e);
+    }
+  f32x16p acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
+  const unsigned long long c0 = clock64(), w0 = wall_clock64();
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) acc[k % 8] = mfma_op<V, E>(a[(k / 2) % 8], b[k % 8], acc[k % 8]);
+  }
+  const unsigned long long c1 = clock64(), w1 = wall_clock64();
+  float z = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) z += acc[i][r];
+  sink[gid] = z;
+  if (threadIdx.x == 0) {
+    clk[2 * blockIdx.x] = c1 - c0;
+    clk[2 * blockIdx.x + 1] = w1 - w0;
+  }
+}
+
+}  // namespace
+
+hipError_t mfma_peak(Act16 t, int blocks, int iters, unsigned long long* clk, float* sink, hipStream_t s) {
+  if (blocks <= 0 || iters <= 0) return hipErrorInvalidValue;
+  if (t == Act16::F16)
+    hipLaunchKernelGGL((mfma_peak_kernel<h16x8, _Float16>), dim3(blocks), dim3(256), 0, s, iters, clk, sink);
+  else
+    hipLaunchKernelGGL((mfma_peak_kernel<b16x8, __bf16>), dim3(blocks), dim3(256), 0, s, iters, clk, sink);
+  return hipGetLastError();
+}
+
+}  // namespace fd

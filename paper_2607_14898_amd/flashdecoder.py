@@ -83,6 +83,8 @@ def load_library() -> ctypes.CDLL:
         "fd_probe_enable": (I32, [P, I32]),
         "fd_probe_read": (I32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64),
                                 ctypes.POINTER(ctypes.c_double)]),
+        "fd_measure_mfma_peak": (I32, [I32, I32, P, ctypes.POINTER(ctypes.c_double),
+                                       ctypes.POINTER(ctypes.c_double)]),
         "fd_status_string": (ctypes.c_char_p, [I32]),
         "fd_last_error": (ctypes.c_char_p, []),
     }
@@ -227,6 +229,14 @@ def fd_probe_read(cache: int):
     ms, n, w = ctypes.c_double(), ctypes.c_int64(), ctypes.c_double()
     _check(load_library().fd_probe_read(cache, ctypes.byref(ms), ctypes.byref(n), ctypes.byref(w)))
     return ms.value, n.value, w.value
+
+
+def fd_measure_mfma_peak(dtype: str = "f16", iters: int = 100000, stream=None):
+    """(TFLOP/s, shader clock GHz) that a dense MFMA load sustains on this GPU."""
+    tf, ghz = ctypes.c_double(), ctypes.c_double()
+    _check(load_library().fd_measure_mfma_peak(_DTYPES[dtype], iters, _stream_handle(stream),
+                                                ctypes.byref(tf), ctypes.byref(ghz)))
+    return tf.value, ghz.value
 
 
 class Decoder:

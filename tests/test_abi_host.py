@@ -93,6 +93,14 @@ def test_struct_size_guard_and_null_arguments():
     assert lib.fd_kv_cache_position(None) == -1
     assert lib.fd_decode_chunk(None, None, 0, 1, None, None, None) == fdb.FD_ERR_INVALID_ARGUMENT
     assert lib.fd_probe_enable(None, 0) == fdb.FD_ERR_INVALID_ARGUMENT
+    d = ctypes.c_double()
+    # argument checks happen before any device call
+    assert lib.fd_measure_mfma_peak(fdb.FD_DTYPE_F32, 10, None, ctypes.byref(d),
+                                    ctypes.byref(d)) == fdb.FD_ERR_INVALID_ARGUMENT
+    assert lib.fd_measure_mfma_peak(fdb.FD_DTYPE_F16, 0, None, ctypes.byref(d),
+                                    ctypes.byref(d)) == fdb.FD_ERR_INVALID_ARGUMENT
+    assert lib.fd_measure_mfma_peak(fdb.FD_DTYPE_F16, 10, None, None,
+                                    None) == fdb.FD_ERR_INVALID_ARGUMENT
     lib.fd_decoder_destroy(None)
     lib.fd_kv_cache_destroy(None)
     assert lib.fd_status_string(fdb.FD_ERR_UNSUPPORTED) == b"unsupported"

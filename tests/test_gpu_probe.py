@@ -1,0 +1,18 @@
+"""The sustained-MFMA probe through the C ABI: the measured throughput and
+clock must be physically plausible for an MI355X (the datasheet dense 16-bit
+peak, 2.5 PFLOP/s at 2.4 GHz, bounds the throughput from above at the
+measured clock)."""
+import pytest
+
+from paper_2607_14898_amd import flashdecoder as fdb
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_mfma_peak_probe_is_plausible(dtype):
+    tf, ghz = fdb.fd_measure_mfma_peak(dtype, 2000)
+    print(f"{dtype}: {tf:.1f} TFLOP/s at {ghz:.3f} GHz", flush=True)
+    assert 0.5 < ghz < 2.6
+    # cannot exceed one 32x32x16 MFMA per 32 cycles per SIMD at the measured clock
+    assert 100.0 < tf <= 2500.0 * ghz / 2.4 * 1.02

@@ -232,11 +232,20 @@ XL_480P = ModelConfig(
     mlp_hidden=6144, head_hidden=6144, s_out=16)
 XL_720P = replace(XL_480P, latent_h=90, latent_w=160)
 
+# FlashDecoder-XL on the Wan2.2 latent space (4x16x16, 48 channels): no
+# PixelUnshuffle (p = 1), so each latent pixel is one token and the same 16x16
+# output pixels per token; the token grids equal the Wan2.1 ones (Sec. 4.3
+# "Generalization", Table 2).
+XL_WAN22_480P = replace(XL_480P, latent_channels=48, latent_h=30, latent_w=52, patch=1)
+XL_WAN22_720P = replace(XL_WAN22_480P, latent_h=45, latent_w=80)
+
 MODELS = {
     "tiny": TINY,
     "tiny-asis": TINY_ASIS,
     "xl-480p": XL_480P,
     "xl-720p": XL_720P,
+    "xl-wan22-480p": XL_WAN22_480P,
+    "xl-wan22-720p": XL_WAN22_720P,
 }
 
 WORKLOADS = {
@@ -246,4 +255,19 @@ WORKLOADS = {
     "xl-480p-stream": Workload("xl-480p-stream", XL_480P, 1, 16, weight_seed=0, latent_seed=103),
     "xl-720p-chunk": Workload("xl-720p-chunk", XL_720P, 4, 1, weight_seed=0, latent_seed=104),
     "xl-720p-stream": Workload("xl-720p-stream", XL_720P, 1, 32, weight_seed=0, latent_seed=105),
+    # the same streams with wider windows: W_frm = 3 and 4 (Table 4) and the
+    # workload list's "previous 3 / 4 chunks" rings (W_frm = 4 at 480p, 5 at 720p)
+    "xl-720p-stream-w3": Workload("xl-720p-stream-w3", replace(XL_720P, window=3), 1, 32,
+                                  weight_seed=0, latent_seed=105),
+    "xl-720p-stream-w4": Workload("xl-720p-stream-w4", replace(XL_720P, window=4), 1, 32,
+                                  weight_seed=0, latent_seed=105),
+    "xl-720p-stream-w5": Workload("xl-720p-stream-w5", replace(XL_720P, window=5), 1, 32,
+                                  weight_seed=0, latent_seed=105),
+    "xl-480p-stream-w4": Workload("xl-480p-stream-w4", replace(XL_480P, window=4), 1, 16,
+                                  weight_seed=0, latent_seed=103),
+    # Wan2.2 latent space (Table 2's second block)
+    "xl-wan22-480p-stream": Workload("xl-wan22-480p-stream", XL_WAN22_480P, 1, 16,
+                                     weight_seed=4, latent_seed=106),
+    "xl-wan22-720p-stream": Workload("xl-wan22-720p-stream", XL_WAN22_720P, 1, 32,
+                                     weight_seed=4, latent_seed=107),
 }

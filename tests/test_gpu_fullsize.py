@@ -50,27 +50,32 @@ def _update_err(x_in, x_gpu, x_ref):
 
 
 def teacher_forced_check(m, Wf, z, out, traces, n_rows=40, log=print):
-    """Checks the decode of chunk 1 (after chunk 0) of latents z [1, C', 2, H', W']
-    from its pixels ``out`` [1, C, 2 r_t, Hs, Ws] and the two per-call residual
-    traces; returns the worst block-update error and the pixel error."""
+    """Checks the decode of the last chunk t of latents z [1, C', t + 1, H', W']
+    streamed one frame per call, from its pixels ``out`` [1, C, (t + 1) r_t, Hs,
+    Ws] and the per-call residual traces: every block's input is the GPU's own
+    (chunk t) and its keys and values come from the GPU's inputs of the visible
+    chunks max(0, t - W + 1) .. t. Returns the worst block-update error and the
+    pixel error."""
     W = {k: np.asarray(v, dtype=np.float64) for k, v in Wf.items()}
     L, r, s, C = m.tokens_per_frame, m.r_t, m.s_out, m.out_channels
-    bb0, rf0 = _split_trace(m, np.asarray(traces[0], dtype=np.float64))
-    bb1, rf1 = _split_trace(m, np.asarray(traces[1], dtype=np.float64))
+    t = len(traces) - 1
+    vis = list(range(max(0, t - m.window + 1), t + 1))
+    split = {c: _split_trace(m, np.asarray(traces[c], dtype=np.float64)) for c in vis}
+    bb1, rf1 = split[t]
     rows = _sample_rows(L, min(n_rows, L), 7)
 
-    # latent projection of chunk 1
-    P = od.pixel_unshuffle_frame(z[0, :, 1].astype(np.float64), m.patch)
+    # latent projection of chunk t
+    P = od.pixel_unshuffle_frame(z[0, :, t].astype(np.float64), m.patch)
     emb = P[rows] @ W["embed.w"].T + W["embed.b"]
     e = np.abs(bb1[0][rows] - emb).max() / np.sqrt(np.mean(emb ** 2))
     log(f"embed: rel max err {e:.2e}")
     assert e < 1e-3
 
-    pos0, pos1 = od.token_positions(m, [0]), od.token_positions(m, [1])
-    pos_k = np.concatenate([pos0, pos1])
+    pos1 = od.token_positions(m, [t])
+    pos_k = np.concatenate([od.token_positions(m, [c]) for c in vis])
     worst = 0.0
     for l in range(m.n_backbone_blocks):
-        xk = np.concatenate([bb0[l], bb1[l]])
+        xk = np.concatenate([split[c][0][l] for c in vis])
         ref = od.block_forward_rows(m, W, f"bb.{l}", xk, pos_k, bb1[l][rows], pos1[rows])
         err = _update_err(bb1[l][rows], bb1[l + 1][rows], ref)
         worst = max(worst, err)
@@ -86,12 +91,11 @@ def teacher_forced_check(m, Wf, z, out, traces, n_rows=40, log=print):
     log(f"temporal up: rel max err {e:.2e}")
     assert e < TOL_UPDATE
 
-    # refinement blocks: keys of all r_t sub-frames of chunks 0 and 1
-    rpos0 = od.token_positions(m, [r * 0 + j for j in range(r)])
-    rpos1 = od.token_positions(m, [r * 1 + j for j in range(r)])
-    rpos_k = np.concatenate([rpos0, rpos1])
+    # refinement blocks: keys of all r_t sub-frames of the visible chunks
+    rpos1 = od.token_positions(m, [r * t + j for j in range(r)])
+    rpos_k = np.concatenate([od.token_positions(m, [r * c + j for j in range(r)]) for c in vis])
     for l in range(m.n_refine_blocks):
-        xk = np.concatenate([rf0[l], rf1[l]])
+        xk = np.concatenate([split[c][1][l] for c in vis])
         ref = od.block_forward_rows(m, W, f"rf.{l}", xk, rpos_k, rf1[l][rrows], rpos1[rrows])
         err = _update_err(rf1[l][rrows], rf1[l + 1][rrows], ref)
         worst = max(worst, err)
@@ -105,20 +109,25 @@ def teacher_forced_check(m, Wf, z, out, traces, n_rows=40, log=print):
     for idx, rr in enumerate(rrows):
         j, n = divmod(int(rr), L)
         h, w = divmod(n, m.grid_w)
-        px = out[0, :, r * 1 + j, s * h:s * h + s, s * w:s * w + s]      # [C, s, s]
+        px = out[0, :, r * t + j, s * h:s * h + s, s * w:s * w + s]      # [C, s, s]
         pe = max(pe, float(np.abs(px.reshape(C * s * s) - f[idx]).max()))
     log(f"pixels: max-abs err {pe:.2e} (worst block update err {worst:.2e})")
     assert pe <= TOL_PIXEL
     return worst, pe
 
 
-@pytest.mark.parametrize("name", ["xl-720p-stream", "xl-480p-stream"])
-def test_stream_teacher_forced_full_size(name):
+@pytest.mark.parametrize("name,chunks", [
+    ("xl-720p-stream", 2), ("xl-480p-stream", 2),
+    # Wan2.2 latent space: 48 channels, no PixelUnshuffle
+    ("xl-wan22-720p-stream", 2),
+    # wider windows: chunk 4 sees chunks 1..4 (W_frm = 4) after the ring wrapped
+    ("xl-480p-stream-w4", 5), ("xl-720p-stream-w4", 5)])
+def test_stream_teacher_forced_full_size(name, chunks):
     wl = WORKLOADS[name]
     m = wl.model
     Wf = wl.weights()
-    z = wl.latents()[:, :, :2]
-    print(f"{name}: decoding 2 chunks with trace", flush=True)
+    z = wl.latents()[:, :, :chunks]
+    print(f"{name}: decoding {chunks} chunks with trace", flush=True)
     out, traces = run_decoder(m, Wf, z, 1, trace=True)
     teacher_forced_check(m, Wf, z, out, traces, log=lambda t: print(t, flush=True))
 

@@ -75,6 +75,31 @@ def test_f16_xl_widths_match_oracle():
     assert _report("xl-narrow f16", got, ref) <= TOL_16
 
 
+def test_f16_wan22_latent_space_matches_oracle():
+    """Wan2.2 latent space: 48 latent channels and no PixelUnshuffle (p = 1), so
+    the embedding reads 48 inputs per token (padded to 64 in K) and each token
+    is one latent pixel."""
+    m = replace(XL_NARROW, latent_channels=48, patch=1, latent_h=10, latent_w=13)
+    W = make_weights(m, 4)
+    z = make_latents(m, 3, 34)
+    ref = decode_stream(m, W, z, 1)
+    got = run_decoder(m, W, z, 1)
+    assert got.shape == (1, 3, 12, 160, 208)
+    assert _report("xl-narrow wan2.2 f16", got, ref) <= TOL_16
+
+
+@pytest.mark.parametrize("window,fpc", [(4, 1), (5, 1), (4, 2)])
+def test_f16_wider_windows_match_oracle(window, fpc):
+    """W_frm = 4 and 5 (Table 4; the workload list's rings of 3 and 4 previous
+    chunks) over 7 frames, so the ring wraps; also calls of 2 frames."""
+    m = replace(XL_NARROW, window=window)
+    W = make_weights(m, 0)
+    z = make_latents(m, 6 if fpc == 2 else 7, 35)
+    ref = decode_stream(m, W, z, 1)
+    got = run_decoder(m, W, z, fpc)
+    assert _report(f"xl-narrow W={window} F={fpc}", got, ref) <= TOL_16
+
+
 def test_f16_xl_widths_unclamped_relative():
     """Pre-clamp head output (clamp off) relative to its RMS, so saturated
     pixels cannot hide errors."""

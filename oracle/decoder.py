@@ -42,7 +42,8 @@ __all__ = [
     "rope_angles", "apply_rope", "attention", "pixel_unshuffle_frame",
     "pixel_shuffle_frame", "band_mask", "StreamingOracle", "decode_full",
     "decode_stream", "block_forward", "token_positions", "block_forward_rows",
-    "stack_final", "temporal_up_rows", "head_rows",
+    "stack_final", "temporal_up_rows", "head_rows", "e4m3_round", "quant_rows_e4m3",
+    "quant_weight_rows_e4m3", "e4m3_decode", "gemm_e4m3",
 ]
 
 # --------------------------------------------------------------------------
@@ -71,6 +72,77 @@ def silu(x: np.ndarray) -> np.ndarray:
 def gelu(x: np.ndarray) -> np.ndarray:
     """GELU, erf form: x * Phi(x)."""
     return 0.5 * x * (1.0 + erf(x / np.sqrt(2.0)))
+
+
+# --------------------------------------------------------------------------
+# FP8 (E4M3) quantisation of the MLP GEMMs (Sec. 4.6: the "-Opt" decoder runs
+# every MLP GEMM in FP8 with static scales)
+# --------------------------------------------------------------------------
+
+E4M3_MAX = 448.0
+
+
+def e4m3_round(x: np.ndarray) -> np.ndarray:
+    """Round to the nearest OCP FP8 E4M3 value (1 sign, 4 exponent bits with
+    bias 7, 3 mantissa bits; normals 2^-6 .. 448 = 1.75 * 2^8, subnormals in
+    steps of 2^-9, no infinities), ties to even, saturating at +-448.
+
+    Within the binade [2^e, 2^(e+1)) of a normal value the spacing is 2^(e-3);
+    below 2^-6 it is the subnormal step 2^-9. Returns float64 values.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    a = np.abs(x)
+    e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
+    # guard the log2 estimate at exact powers of two / rounding of log2
+    e = np.where(2.0 ** e > a, e - 1, e)
+    e = np.where(2.0 ** (e + 1) <= a, e + 1, e)
+    quantum = 2.0 ** (np.maximum(e, -6.0) - 3.0)       # subnormals share 2^-9
+    q = np.rint(a / quantum) * quantum                 # rint: ties to even
+    q = np.minimum(q, E4M3_MAX)
+    return np.where(a > 0, np.copysign(q, x), 0.0 * x)
+
+
+def quant_rows_e4m3(a: np.ndarray):
+    """Per-row (per-token) quantisation of activations [M, K]: the row's
+    amplitude m = max|a| (in fp32, as the kernels hold the row), inv = 448 / m,
+    codes e4m3(fp32(a * inv)), dequantisation scale s = fp32(m / 448) (1 for an
+    all-zero row). Returns (codes as float64 [M, K], s [M] float64)."""
+    a32 = np.asarray(a, dtype=np.float32)
+    m = np.max(np.abs(a32), axis=-1)
+    safe = np.where(m > 0, m, np.float32(448.0)).astype(np.float32)
+    inv = (np.float32(448.0) / safe).astype(np.float32)
+    codes = e4m3_round((a32 * inv[:, None]).astype(np.float32))
+    s = (safe / np.float32(448.0)).astype(np.float32)
+    return codes, s.astype(np.float64)
+
+
+def quant_weight_rows_e4m3(w: np.ndarray):
+    """Per-output-channel quantisation of a weight [N, K]: the same rule as
+    quant_rows_e4m3 applied to each row of W (the static weight scales)."""
+    return quant_rows_e4m3(w)
+
+
+def e4m3_decode(codes: np.ndarray) -> np.ndarray:
+    """Value of OCP E4M3 byte codes from their bit fields: bit 7 the sign,
+    bits 6..3 the exponent E (bias 7), bits 2..0 the mantissa M; E = 0 is
+    subnormal, M/8 * 2^-6; S.1111.111 is NaN (nan here). float64."""
+    c = np.asarray(codes).astype(np.int64)
+    sign = np.where(c & 0x80, -1.0, 1.0)
+    e, m = (c >> 3) & 0xF, c & 0x7
+    mag = np.where(e == 0, m / 8.0 * 2.0 ** -6, (1.0 + m / 8.0) * 2.0 ** (e - 7.0))
+    mag = np.where((e == 15) & (m == 7), np.nan, mag)
+    return sign * mag
+
+
+def gemm_e4m3(a_codes: np.ndarray, a_scale: np.ndarray, w_codes: np.ndarray,
+              w_scale: np.ndarray, bias: np.ndarray) -> np.ndarray:
+    """E4M3 GEMM with per-row (activation) and per-column (weight channel)
+    dequantisation, by definition: C[m, n] = (sum_k dec(a[m, k]) dec(w[n, k]))
+    * a_scale[m] * w_scale[n] + bias[n], in float64 (a_codes [M, K] and
+    w_codes [N, K] are byte codes)."""
+    acc = e4m3_decode(a_codes) @ e4m3_decode(w_codes).T
+    return acc * np.asarray(a_scale, np.float64)[:, None] * \
+        np.asarray(w_scale, np.float64)[None, :] + np.asarray(bias, np.float64)[None, :]
 
 
 # --------------------------------------------------------------------------
@@ -214,9 +286,29 @@ def _qkv(cfg, W, p: str, a: np.ndarray, pos: np.ndarray):
     return q, k, v
 
 
+def _fp8_linear(x: np.ndarray, w: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """x W^T + b with x quantised per row and W per output channel to E4M3:
+    (codes_x codes_W^T) * s_x[:, None] * s_W[None, :] + b."""
+    qx, sx = quant_rows_e4m3(x)
+    qw, sw = quant_weight_rows_e4m3(w)
+    return (qx @ qw.T) * sx[:, None] * sw[None, :] + b
+
+
 def _mlp(cfg, W, p: str, a: np.ndarray) -> np.ndarray:
     """Reading: SwiGLU with hidden width mlp_hidden (rows gate | up of w13);
-    the GELU form is the plain two-matrix MLP."""
+    the GELU form is the plain two-matrix MLP.
+
+    With cfg.mlp_precision == "fp8" (the "-Opt" variant of Sec. 4.6) both MLP
+    GEMMs take E4M3 operands: the MLP input per token, the weights per output
+    channel, and the SwiGLU output per token after it is stored in fp16 (the
+    precision the hidden activation is kept in between the two GEMMs)."""
+    if getattr(cfg, "mlp_precision", "f16") == "fp8":
+        if cfg.mlp_kind != "swiglu":
+            raise ValueError("the FP8 MLP is defined for the SwiGLU form")
+        H = cfg.mlp_hidden
+        y = _fp8_linear(a, W[p + ".w13"], W[p + ".b13"])
+        h = (silu(y[:, :H]) * y[:, H:]).astype(np.float16).astype(np.float64)
+        return _fp8_linear(h, W[p + ".w2"], W[p + ".b2"])
     if cfg.mlp_kind == "swiglu":
         H = cfg.mlp_hidden
         y = a @ W[p + ".w13"].T + W[p + ".b13"]

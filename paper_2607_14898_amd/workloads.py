@@ -58,6 +58,7 @@ class ModelConfig:
     unit_frames: int = 1        # latent frames per causal unit
     out_channels: int = 3       # C (RGB)
     clamp_output: bool = True
+    mlp_precision: str = "f16"  # "f16" (the compute dtype) | "fp8" (E4M3 MLP GEMMs, Sec. 4.6)
 
     @property
     def head_dim(self) -> int:
@@ -265,6 +266,13 @@ WORKLOADS = {
                                   weight_seed=0, latent_seed=105),
     "xl-480p-stream-w4": Workload("xl-480p-stream-w4", replace(XL_480P, window=4), 1, 16,
                                   weight_seed=0, latent_seed=103),
+    # the FP8-MLP ("-Opt", Sec. 4.6) decoder on the same streams
+    "xl-720p-stream-fp8": Workload("xl-720p-stream-fp8", replace(XL_720P, mlp_precision="fp8"), 1, 32,
+                                   weight_seed=0, latent_seed=105),
+    "xl-480p-stream-fp8": Workload("xl-480p-stream-fp8", replace(XL_480P, mlp_precision="fp8"), 1, 16,
+                                   weight_seed=0, latent_seed=103),
+    "xl-720p-chunk-fp8": Workload("xl-720p-chunk-fp8", replace(XL_720P, mlp_precision="fp8"), 4, 1,
+                                  weight_seed=0, latent_seed=104),
     # Wan2.2 latent space (Table 2's second block)
     "xl-wan22-480p-stream": Workload("xl-wan22-480p-stream", XL_WAN22_480P, 1, 16,
                                      weight_seed=4, latent_seed=106),

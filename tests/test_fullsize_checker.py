@@ -59,3 +59,42 @@ def test_teacher_forced_checker_catches_planted_errors(plant):
         out[0, :, 4 * 3 + 1] = np.clip(out[0, :, 4 * 3 + 1] + 0.05, -1.0, 1.0)
     with pytest.raises(AssertionError):
         teacher_forced_check(m, W, z, out, traces, n_rows=20, log=lambda t: None)
+
+
+def _fp8_traces(m, W, z, chunks, W_gen=None):
+    orc = StreamingOracle(m, W if W_gen is None else W_gen)
+    traces, outs = [], []
+    for t in range(chunks):
+        orc.trace = []
+        outs.append(orc.decode(z[0, :, t:t + 1]))
+        traces.append(np.concatenate([x.ravel() for _, _, x in orc.trace]))
+    return np.concatenate(outs, axis=1)[None], traces
+
+
+FP8_SMALL = dict(latent_h=12, latent_w=20, n_backbone_blocks=2, n_refine_blocks=1,
+                 compute_dtype="f16", mlp_precision="fp8", dim=256, n_heads=4, n_kv_groups=2,
+                 mlp_hidden=512, head_hidden=512, window=2)
+
+
+def test_teacher_forced_checker_fp8_on_oracle_traces():
+    """The FP8-MLP branch (tolerance calibrated on the oracle's own spread)
+    accepts the fake-quant oracle's traces."""
+    m = replace(MODELS["xl-720p"], **FP8_SMALL)
+    W = make_weights(m, 3)
+    z = make_latents(m, 2, 4)
+    out, traces = _fp8_traces(m, W, z, 2)
+    worst, pe = teacher_forced_check(m, W, z, out, traces, n_rows=20, log=lambda t: None)
+    assert worst < 1e-10 and pe < 1e-10
+
+
+def test_teacher_forced_checker_fp8_catches_a_wrong_channel_scale():
+    """Traces made with one block's down-projection off by 5% (as a wrong
+    per-channel scale would make them) fail the FP8 branch."""
+    m = replace(MODELS["xl-720p"], **FP8_SMALL)
+    W = make_weights(m, 3)
+    z = make_latents(m, 2, 4)
+    Wbad = dict(W)
+    Wbad["bb.1.w2"] = W["bb.1.w2"] * 1.05
+    out, traces = _fp8_traces(m, W, z, 2, W_gen=Wbad)
+    with pytest.raises(AssertionError, match="bb.1"):
+        teacher_forced_check(m, W, z, out, traces, n_rows=20, log=lambda t: None)

@@ -11,6 +11,12 @@ The embedding, the temporal upsampling and the pixel head are checked the same
 way, the head on the final clamped pixels at 2e-2 max-abs. Properties that hold
 at any size are checked at full size too: a 4-frame call equals 4 streamed
 calls bit for bit, causality, and determinism.
+
+With the FP8 MLP the oracle block fake-quantises the MLP the same way, and
+each block's tolerance is calibrated on the oracle itself: the block rerun
+with its inputs perturbed by relative 2^-11 (the 16-bit path's rounding, from
+which the kernels decide their E4M3 codes) moves the update by a spread s;
+the GPU must stay within max(2e-2, 2 s) at the maximum and 1.5 s on average.
 """
 import numpy as np
 import pytest
@@ -43,10 +49,34 @@ def _sample_rows(L, n, seed):
     return np.array(sorted(rows))
 
 
+NOISE = 2.0 ** -11
+
+
 def _update_err(x_in, x_gpu, x_ref):
+    """(max, mean) of |delta_gpu - delta_ref| / rms(delta_ref)."""
     d_ref = x_ref - x_in
-    d_gpu = x_gpu - x_in
-    return float(np.abs(d_gpu - d_ref).max() / np.sqrt(np.mean(d_ref ** 2)))
+    d = np.abs((x_gpu - x_in) - d_ref) / np.sqrt(np.mean(d_ref ** 2))
+    return float(d.max()), float(d.mean())
+
+
+def _check_block(m, W, p, xk, pos_k, qidx, pos_q, x_gpu, log):
+    """One block teacher-forced: keys / values from xk, query rows xk[qidx];
+    returns the worst relative update error after asserting the tolerance."""
+    ref = od.block_forward_rows(m, W, p, xk, pos_k, xk[qidx], pos_q)
+    err, mean = _update_err(xk[qidx], x_gpu, ref)
+    if getattr(m, "mlp_precision", "f16") != "fp8":
+        log(f"{p}: update err {err:.2e}")
+        assert err < TOL_UPDATE, (p, err)
+        return err
+    rng = np.random.default_rng(len(p) * 1000 + int(p.split(".")[1]))
+    xp = xk * (1.0 + NOISE * rng.uniform(-1.0, 1.0, xk.shape))
+    refp = od.block_forward_rows(m, W, p, xp, pos_k, xp[qidx], pos_q)
+    d_ref = ref - xk[qidx]
+    sp = np.abs((refp - xp[qidx]) - d_ref) / np.sqrt(np.mean(d_ref ** 2))
+    log(f"{p}: update err max {err:.2e} mean {mean:.2e}; oracle spread max {sp.max():.2e} "
+        f"mean {sp.mean():.2e}")
+    assert err <= max(TOL_UPDATE, 2.0 * sp.max()) and mean <= 1.5 * sp.mean(), (p, err, mean)
+    return err
 
 
 def teacher_forced_check(m, Wf, z, out, traces, n_rows=40, log=print):
@@ -74,13 +104,12 @@ def teacher_forced_check(m, Wf, z, out, traces, n_rows=40, log=print):
     pos1 = od.token_positions(m, [t])
     pos_k = np.concatenate([od.token_positions(m, [c]) for c in vis])
     worst = 0.0
+    qidx = (len(vis) - 1) * L + rows            # chunk t's sampled rows inside the key rows
     for l in range(m.n_backbone_blocks):
         xk = np.concatenate([split[c][0][l] for c in vis])
-        ref = od.block_forward_rows(m, W, f"bb.{l}", xk, pos_k, bb1[l][rows], pos1[rows])
-        err = _update_err(bb1[l][rows], bb1[l + 1][rows], ref)
+        assert np.array_equal(xk[qidx], bb1[l][rows])
+        err = _check_block(m, W, f"bb.{l}", xk, pos_k, qidx, pos1[rows], bb1[l + 1][rows], log)
         worst = max(worst, err)
-        log(f"bb.{l}: update err {err:.2e}")
-        assert err < TOL_UPDATE, (l, err)
 
     # temporal upsampling from the backbone output
     y = od.stack_final(m, W, "bb", bb1[m.n_backbone_blocks][rows])
@@ -94,13 +123,12 @@ def teacher_forced_check(m, Wf, z, out, traces, n_rows=40, log=print):
     # refinement blocks: keys of all r_t sub-frames of the visible chunks
     rpos1 = od.token_positions(m, [r * t + j for j in range(r)])
     rpos_k = np.concatenate([od.token_positions(m, [r * c + j for j in range(r)]) for c in vis])
+    rqidx = (len(vis) - 1) * r * L + rrows
     for l in range(m.n_refine_blocks):
         xk = np.concatenate([split[c][1][l] for c in vis])
-        ref = od.block_forward_rows(m, W, f"rf.{l}", xk, rpos_k, rf1[l][rrows], rpos1[rrows])
-        err = _update_err(rf1[l][rrows], rf1[l + 1][rrows], ref)
+        assert np.array_equal(xk[rqidx], rf1[l][rrows])
+        err = _check_block(m, W, f"rf.{l}", xk, rpos_k, rqidx, rpos1[rrows], rf1[l + 1][rrows], log)
         worst = max(worst, err)
-        log(f"rf.{l}: update err {err:.2e}")
-        assert err < TOL_UPDATE, (l, err)
 
     # pixel head + PixelShuffle + clamp, from the refinement output
     yr = od.stack_final(m, W, "rf", rf1[m.n_refine_blocks][rrows])
@@ -121,7 +149,9 @@ def teacher_forced_check(m, Wf, z, out, traces, n_rows=40, log=print):
     # Wan2.2 latent space: 48 channels, no PixelUnshuffle
     ("xl-wan22-720p-stream", 2),
     # wider windows: chunk 4 sees chunks 1..4 (W_frm = 4) after the ring wrapped
-    ("xl-480p-stream-w4", 5), ("xl-720p-stream-w4", 5)])
+    ("xl-480p-stream-w4", 5), ("xl-720p-stream-w4", 5),
+    # the FP8-MLP decoder
+    ("xl-720p-stream-fp8", 2)])
 def test_stream_teacher_forced_full_size(name, chunks):
     wl = WORKLOADS[name]
     m = wl.model

@@ -375,3 +375,150 @@ def test_row_subset_block_equals_full_block():
     t = odm.temporal_up_rows(cfg, W, y[rows])
     full_t = odm._temporal_up(cfg, W, y, 1).reshape(cfg.r_t, L, cfg.dim)
     np.testing.assert_allclose(t, full_t[:, rows].transpose(1, 0, 2), atol=1e-12, rtol=0)
+
+
+# --------------------------------------------------------------------------
+# FP8 (E4M3) MLP of the "-Opt" decoder (Sec. 4.6): pins of the fake-quant oracle
+# --------------------------------------------------------------------------
+
+def _e4m3_table():
+    """Every finite OCP E4M3 value, built from the bit fields: sign S, exponent
+    E (bias 7), mantissa M; E = 0 is subnormal (M/8 * 2^-6); S.1111.111 is NaN."""
+    out = []
+    for sgn in (1.0, -1.0):
+        for e in range(16):
+            for m in range(8):
+                if e == 15 and m == 7:
+                    continue
+                v = (m / 8.0) * 2.0 ** -6 if e == 0 else (1.0 + m / 8.0) * 2.0 ** (e - 7)
+                out.append((sgn * v, m))
+    return out
+
+
+def test_e4m3_codes_are_fixed_points_and_extremes():
+    from oracle.decoder import e4m3_round
+    tab = _e4m3_table()
+    vals = np.array([v for v, _ in tab])
+    assert len(set(np.abs(vals).tolist())) == 127          # 0 and 126 magnitudes
+    assert np.array_equal(e4m3_round(vals), vals)
+    assert np.abs(vals).max() == 448.0 and np.abs(vals[vals != 0]).min() == 2.0 ** -9
+    assert np.array_equal(e4m3_round(np.array([449.0, 1e6, -500.0, np.float32(3e38)])),
+                          np.array([448.0, 448.0, -448.0, 448.0]))
+
+
+def test_e4m3_round_equals_brute_force_nearest_ties_to_even():
+    """Against a search over the whole code table: the nearest value; at an
+    exact midpoint, the one with an even mantissa field."""
+    from oracle.decoder import e4m3_round
+    tab = _e4m3_table()
+    vals = np.array([v for v, _ in tab])
+    mant = np.array([m for _, m in tab])
+    pos = np.unique(np.abs(vals))
+    mids = (pos[1:] + pos[:-1]) / 2.0
+    rng = np.random.default_rng(5)
+    xs = np.concatenate([mids, -mids, rng.standard_normal(4000) * 20.0,
+                         rng.standard_normal(2000) * 0.01, np.nextafter(mids, 0), np.nextafter(mids, 1e9)])
+    xs = xs[np.abs(xs) <= 448.0]
+    got = e4m3_round(xs)
+    for x, g in zip(xs, got):
+        d = np.abs(vals - x)
+        best = np.flatnonzero(d == d.min())
+        if len(best) > 1:                                   # tie: the even mantissa
+            best = [b for b in best if mant[b] % 2 == 0]
+        assert g == vals[best[0]], (x, g, vals[best])
+
+
+def test_fp8_row_quantisation_invariants():
+    from oracle.decoder import quant_rows_e4m3
+    rng = np.random.default_rng(6)
+    a = rng.standard_normal((7, 96)) * np.array([[1e-3], [0.1], [1], [10], [300], [1], [1]])
+    a[6] = 0.0
+    q, s = quant_rows_e4m3(a)
+    assert np.all(np.abs(q) <= 448.0)
+    np.testing.assert_allclose(np.abs(q[:6]).max(axis=1), 448.0)   # the row maximum maps to 448
+    deq = q * s[:, None]
+    rel = np.abs(deq - a)[:6] / np.abs(a[:6]).max(axis=1, keepdims=True)
+    assert rel.max() <= 2.0 ** -4 * 1.001                           # half a step of the top binade
+    assert np.all(q[6] == 0) and s[6] == 1.0
+
+
+def test_fp8_linear_matches_a_scalar_loop():
+    """The fake-quant GEMM is the plain sum over codes times both scales."""
+    from oracle.decoder import _fp8_linear, e4m3_round
+    rng = np.random.default_rng(7)
+    x, w, b = rng.standard_normal((3, 5)), rng.standard_normal((4, 5)) * 0.05, rng.standard_normal(4)
+    got = _fp8_linear(x, w, b)
+    for i in range(3):
+        x32 = x[i].astype(np.float32)
+        sx = np.float32(np.abs(x32).max()) / np.float32(448.0)
+        ix = np.float32(448.0) / np.float32(np.abs(x32).max())
+        for n in range(4):
+            w32 = w[n].astype(np.float32)
+            sw = np.float32(np.abs(w32).max()) / np.float32(448.0)
+            iw = np.float32(448.0) / np.float32(np.abs(w32).max())
+            acc = 0.0
+            for k in range(5):
+                acc += float(e4m3_round(np.float32(x32[k] * ix))) * float(e4m3_round(np.float32(w32[k] * iw)))
+            assert abs(got[i, n] - (acc * float(sx) * float(sw) + b[n])) < 1e-12
+
+
+def test_fp8_mlp_decoder_stays_close_to_the_16bit_one():
+    """The FP8 MLP changes the output by quantisation noise only (a planted
+    mistake, e.g. a dropped scale, moves it by O(1))."""
+    from dataclasses import replace as rp
+    m = rp(MODELS["tiny"], compute_dtype="f16", latent_h=6, latent_w=10)
+    m8 = rp(m, mlp_precision="fp8")
+    W = make_weights(m, 8, std=0.05)
+    z = make_latents(m, 3, 9)
+    a = decode_stream(m, W, z, 1)
+    b = decode_stream(m8, W, z, 1)
+    d = np.abs(a - b)
+    assert 1e-3 < d.max() < 0.25 and d.mean() < 0.03, (d.max(), d.mean())
+
+
+def test_e4m3_decode_is_the_code_table_and_inverts_the_rounding():
+    """Every byte decodes to the table value of its bit fields (built above by
+    a separate loop), NaN codes to nan, and rounding a decoded value returns it."""
+    from oracle.decoder import e4m3_decode, e4m3_round
+    codes = np.arange(256, dtype=np.uint8)
+    v = e4m3_decode(codes)
+    assert np.isnan(v[0x7F]) and np.isnan(v[0xFF]) and np.isnan(v).sum() == 2
+    tab = _e4m3_table()                        # positive codes 0..126, then negative
+    want = np.array([t for t, _ in tab])
+    got = np.concatenate([v[:127], v[128:255]])
+    assert np.array_equal(got, want)
+    fin = ~np.isnan(v)
+    assert np.array_equal(e4m3_round(v[fin]), v[fin])
+    assert v[0x38] == 1.0 and v[0xB8] == -1.0 and v[0x7E] == 448.0 and v[0x01] == 2.0 ** -9
+    assert np.all(np.diff(v[:127]) > 0)        # codes 0..126 are ordered by value
+
+
+def test_e4m3_gemm_matches_a_scalar_loop_and_the_fake_quant_linear():
+    """gemm_e4m3 on codes equals a triple loop over the bit-field table, and
+    fed the codes and scales of quant_rows_e4m3 it is the fake-quant linear."""
+    from oracle.decoder import gemm_e4m3, quant_rows_e4m3, _fp8_linear
+    tab = {}
+    for code in range(256):
+        s, e, m = code >> 7, (code >> 3) & 15, code & 7
+        if e == 15 and m == 7:
+            continue
+        mag = m * 2.0 ** -9 if e == 0 else (8 + m) * 2.0 ** (e - 10)
+        tab[code] = -mag if s else mag
+    rng = np.random.default_rng(17)
+    ok = np.array(sorted(tab))
+    a = rng.choice(ok, (3, 6)).astype(np.uint8)
+    w = rng.choice(ok, (4, 6)).astype(np.uint8)
+    sa, sw, b = rng.uniform(0.1, 2, 3), rng.uniform(0.1, 2, 4), rng.standard_normal(4)
+    got = gemm_e4m3(a, sa, w, sw, b)
+    for i in range(3):
+        for n in range(4):
+            acc = sum(tab[int(a[i, k])] * tab[int(w[n, k])] for k in range(6))
+            assert abs(got[i, n] - (acc * sa[i] * sw[n] + b[n])) < 1e-12
+    x, wf = rng.standard_normal((5, 64)), rng.standard_normal((7, 64)) * 0.05
+    qx, sx = quant_rows_e4m3(x)
+    qw, sww = quant_rows_e4m3(wf)
+    inv = {v: c for c, v in tab.items() if not (v == 0 and c == 0x80)}
+    cx = np.vectorize(inv.get)(qx).astype(np.uint8)
+    cw = np.vectorize(inv.get)(qw).astype(np.uint8)
+    bb = rng.standard_normal(7)
+    np.testing.assert_allclose(gemm_e4m3(cx, sx, cw, sww, bb), _fp8_linear(x, wf, bb), rtol=0, atol=1e-12)

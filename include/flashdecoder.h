@@ -45,6 +45,14 @@ typedef enum fd_dtype { FD_DTYPE_F32 = 0, FD_DTYPE_BF16 = 1, FD_DTYPE_F16 = 2 } 
 enum { FD_MLP_SWIGLU = 0, FD_MLP_GELU = 1 };
 enum { FD_NORM_RMS = 0, FD_NORM_LAYER = 1 };
 enum { FD_HEAD_TEMPORAL_FIRST = 0, FD_HEAD_LINEAR = 1 };
+/* Operand precision of the two MLP GEMMs of every block. FP8: the "-Opt"
+ * decoder of Sec. 4.6 runs its MLP GEMMs in FP8; here both take OCP E4M3
+ * operands (round to nearest even, saturating at +-448): the weights quantised
+ * per output channel at create (static scales), the MLP input and the SwiGLU
+ * output (kept in fp16 between the two GEMMs) per token when produced, with
+ * fp32 accumulation and the two scales applied in the epilogue. Needs a 16-bit
+ * compute dtype and the SwiGLU MLP. */
+enum { FD_MLP_PRECISION_COMPUTE = 0, FD_MLP_PRECISION_FP8 = 1 };
 
 /* Decoder shape. Copied by fd_decoder_create; the caller keeps ownership.
  * Field meanings follow the paper's notation (Sec. 3.2-3.4, supplement Table A). */
@@ -76,6 +84,7 @@ typedef struct fd_config {
   int32_t max_batch;         /* largest batch a cache of this decoder may hold           */
   int32_t max_frames_per_call;/* largest n_frames of one fd_decode_chunk call            */
   int32_t clamp_output;      /* 1: clamp pixels to [-1, 1]                               */
+  int32_t mlp_precision;     /* FD_MLP_PRECISION_*                                       */
 } fd_config;
 
 /* One learned tensor of the canonical weight blob. */
@@ -197,6 +206,61 @@ fd_status fd_probe_read(fd_kv_cache* cache, double* total_ms, int64_t* launches,
  * else INVALID_ARGUMENT; HIP failures give DEVICE. */
 fd_status fd_measure_mfma_peak(int32_t dtype, int32_t iters, void* stream, double* tflops,
                                double* clock_ghz);
+
+/* E4M3 quantisation of rows, the rule the FP8 MLP applies to its weights
+ * (FD_MLP_PRECISION_FP8): for each row r of in[rows][cols] (row-major fp32),
+ * m = max |in[r][:]|, inv = 448 / m (fp32 division), codes[r][c] = the OCP
+ * E4M3 code nearest to fp32(in[r][c] * inv), ties to even, saturating at
+ * +-448 (bit layout S.EEEE.MMM, exponent bias 7); scales[r] = m / 448 (fp32),
+ * so in ~= decode(codes) * scales. A row of zeros gives codes 0 and scale 1.
+ * Host pointers, caller-owned; rows >= 0, cols >= 1, else INVALID_ARGUMENT.
+ * NaN or infinite inputs give INVALID_ARGUMENT. */
+fd_status fd_quantize_e4m3_rows(const float* in, int64_t rows, int64_t cols, uint8_t* codes,
+                                float* scales);
+
+/* The same rule on the GPU (the kernel the FP8 MLP uses for its per-token
+ * activation codes), on device pointers in[rows][cols] fp32, codes[rows][cols]
+ * bytes and scales[rows] fp32, enqueued on `stream` (NULL = default);
+ * asynchronous. cols a multiple of 8 in [8, 65536], rows >= 0, else
+ * INVALID_ARGUMENT. */
+fd_status fd_quantize_e4m3_rows_device(const float* in, int64_t rows, int64_t cols, uint8_t* codes,
+                                       float* scales, void* stream);
+
+/* Packing of an E4M3 weight for fd_gemm_e4m3_device (the layout the FP8 MLP
+ * keeps its weights in): w[n][k] (row-major byte codes, host) goes to 1 KB
+ * blocks of 16 rows x 64 K-columns, block (n / 16, k / 64) at byte offset
+ * ((n / 16) (K / 64) + k / 64) 1024, inside it row n % 16 at 64 (n % 16) and
+ * column k % 64; rows up to the next multiple of 16 are zero. packed (host,
+ * caller-owned) holds ceil(N / 16) 16 K bytes. N >= 1, K a positive multiple
+ * of 64, non-NULL pointers, else INVALID_ARGUMENT. */
+fd_status fd_pack_e4m3_weight(const uint8_t* w, int64_t n, int64_t k, uint8_t* packed);
+
+/* Epilogues of fd_gemm_e4m3_device. */
+enum {
+  /* out is fp32 [M][ld_out]: out[m][c] += C[m][c] for c < N */
+  FD_GEMM_E4M3_RESID_ADD = 0,
+  /* SwiGLU: W rows interleaved per 32 (rows 64 i .. 64 i + 31 gate, 64 i + 32
+   * .. 64 i + 63 up); out is fp16 [M][ld_out]:
+   * out[m][32 i + j] = fp16(SiLU(C[m][64 i + j]) C[m][64 i + 32 + j]) */
+  FD_GEMM_E4M3_SWIGLU_F16 = 1
+};
+
+/* The E4M3 GEMM the FP8 MLP's two projections run on (Sec. 4.6, the "-Opt"
+ * decoder's FP8 MLP GEMMs), on the gfx950 FP8 matrix cores:
+ *   C[m][n] = (sum_k e4m3(a[m][k]) e4m3(w[n][k])) a_scale[m] w_scale[n] + bias[n]
+ * with fp32 accumulation (each product is exact in fp32), then the epilogue.
+ * Device pointers: a [M][lda] E4M3 codes (16-byte aligned, lda a multiple of
+ * 16, lda >= K), a_scale [M], w_packed as fd_pack_e4m3_weight writes it
+ * (16-byte aligned), w_scale [N], bias [N] (fp32), out per the epilogue
+ * (SwiGLU: N a multiple of 64, ld_out >= N / 2 and a multiple of 4, out
+ * 8-byte aligned; residual add: ld_out >= N). M >= 0, 1 <= N, K a multiple of
+ * 64 in [64, 65536], lda and ld_out below 2^20, else INVALID_ARGUMENT.
+ * Enqueued on `stream` (NULL = default), asynchronous; a launch failure gives
+ * DEVICE. */
+fd_status fd_gemm_e4m3_device(const uint8_t* a, int64_t lda, const float* a_scale,
+                              const uint8_t* w_packed, const float* w_scale, const float* bias,
+                              int32_t m, int32_t n, int32_t k, int32_t epilogue, void* out,
+                              int64_t ld_out, void* stream);
 
 const char* fd_status_string(fd_status status);
 

@@ -60,6 +60,10 @@ struct EpiParams {
   int frames_in = 0;        // latent frames in the call
   int frames_out = 0;       // output frames in the call (frames_in * r_t)
   int clamp = 1;
+  // FP8 GEMM: the accumulator of (row m, column n) is multiplied by
+  // row_scale[m] * col_scale[n] before the bias and the epilogue
+  const float* row_scale = nullptr;
+  const float* col_scale = nullptr;
   QkvPostArgs qkv;          // EPI_QKV geometry and destinations (raw unused)
 };
 
@@ -80,11 +84,22 @@ struct GemmArgs {
 inline int64_t pack_w16_index(int64_t row, int64_t k, int64_t K) {
   return ((row / 16) * (K / 32) + k / 32) * 512 + (row % 16) * 32 + k % 32;
 }
+// Position of byte (row, k) of an [N, K] E4M3 weight in the packed layout the
+// FP8 MFMA GEMM reads: 1 KB blocks of 16 rows x 64 K-columns, block-row major,
+// rows padded with zeros to a multiple of 16.
+inline int64_t pack_w8_index(int64_t row, int64_t k, int64_t K) {
+  return ((row / 16) * (K / 64) + k / 64) * 1024 + (row % 16) * 64 + k % 64;
+}
 // 16-bit operand GEMM on MFMA (K > 0, K % 32 == 0, lda % 8 == 0, 16-byte aligned
 // A; W packed as above).
 hipError_t gemm_mfma(Act16 t, const GemmArgs& g, hipStream_t stream);
 // fp32 GEMM (any shape) for the fp32 compute path.
 hipError_t gemm_f32(const GemmArgs& g, hipStream_t stream);
+// E4M3 x E4M3 GEMM on the gfx950 32x32x64 FP8 MFMA: A [M, K] E4M3 bytes
+// row-major (lda bytes, lda % 16 == 0), W packed by pack_w8_index, K % 64 == 0;
+// epilogues EPI_SWIGLU (fp16 out_a) and EPI_RESID_ADD, after the row / column
+// scales of EpiParams.
+hipError_t gemm_fp8(const GemmArgs& g, hipStream_t stream);
 
 // Attention over the rolling KV ring.
 struct AttnArgs {
@@ -104,9 +119,16 @@ hipError_t attention_mfma(Act16 t, const AttnArgs& a, hipStream_t stream);
 hipError_t attention_f32(const AttnArgs& a, hipStream_t stream);
 
 // Norm of the fp32 residual stream into the next GEMM's operand format.
-// kind 0 = RMSNorm, 1 = LayerNorm. out_kind: 0 f16, 1 bf16, 2 fp32.
+// kind 0 = RMSNorm, 1 = LayerNorm. out_kind: 0 f16, 1 bf16, 2 fp32, 3 E4M3
+// codes with the per-row scale (rule of fd_quantize_e4m3_rows) in row_scale.
 hipError_t norm_rows(const float* x, int M, int D, const float* g, const float* b, int kind,
-                     float eps, void* out, int out_kind, hipStream_t stream);
+                     float eps, void* out, int out_kind, hipStream_t stream,
+                     float* row_scale = nullptr);
+
+// Per-row E4M3 quantisation (rule of fd_quantize_e4m3_rows) of in [M, K]
+// (in_kind 0 f16, 2 fp32) into codes [M, K] bytes and scale [M] fp32.
+hipError_t quant_rows_e4m3(const void* in, int in_kind, int64_t M, int K, uint8_t* codes,
+                           float* scale, hipStream_t stream);
 
 // Split raw qkv (fp32, bias included) into rotated queries and the KV ring
 // (KV-norm, RoPE) for rows of one call.

@@ -39,6 +39,7 @@ fd_status fail(fd_status st, const char* fmt, ...) {
 struct Derived {
   int Dh, grid_h, grid_w, L, K_in, K_pad, qkv_w, act_bytes;
   bool is16;
+  bool mlp8;     // MLP GEMMs on E4M3 operands (FD_MLP_PRECISION_FP8)
   fd::Act16 a16;
   int act_kind;  // 0 f16, 1 bf16, 2 fp32
 };
@@ -77,6 +78,8 @@ fd_status validate(const fd_config* c, Derived* d) {
     return fail(FD_ERR_INVALID_ARGUMENT, "norm_eps must be > 0 and rope_theta > 1");
   if (c->max_frames_per_call % c->unit_frames)
     return fail(FD_ERR_INVALID_ARGUMENT, "max_frames_per_call must be a multiple of unit_frames");
+  if (c->mlp_precision != FD_MLP_PRECISION_COMPUTE && c->mlp_precision != FD_MLP_PRECISION_FP8)
+    return fail(FD_ERR_INVALID_ARGUMENT, "unknown mlp_precision");
   Derived x{};
   x.Dh = c->dim / c->n_heads;
   x.grid_h = c->latent_h / c->patch;
@@ -103,6 +106,9 @@ fd_status validate(const fd_config* c, Derived* d) {
   } else if (x.Dh != 16 && x.Dh != 32 && x.Dh != 64) {
     return fail(FD_ERR_UNSUPPORTED, "fp32 compute needs D_h in {16, 32, 64}");
   }
+  x.mlp8 = c->mlp_precision == FD_MLP_PRECISION_FP8;
+  if (x.mlp8 && (!x.is16 || c->mlp_kind != FD_MLP_SWIGLU))
+    return fail(FD_ERR_UNSUPPORTED, "the FP8 MLP needs a 16-bit compute dtype and the SwiGLU MLP");
   if (d) *d = x;
   return FD_OK;
 }
@@ -190,7 +196,45 @@ struct LayerW {
   const void *wqkv = nullptr, *wo = nullptr, *w1 = nullptr, *w2 = nullptr;
   const float *n1g = nullptr, *n1b = nullptr, *bqkv = nullptr, *kg = nullptr, *vg = nullptr,
               *bo = nullptr, *n2g = nullptr, *n2b = nullptr, *b1 = nullptr, *b2 = nullptr;
+  const float *s1 = nullptr, *s2 = nullptr;  // per-output-channel scales of E4M3 w13 / w2
 };
+
+// OCP E4M3 code (bit layout S.EEEE.MMM, exponent bias 7, no infinities) of a
+// finite value: the nearest representable value, ties to even, saturating at
+// +-448. Normals 2^e (1 + M/8) for e = -6..8; below 2^-6 subnormals M 2^-9.
+uint8_t e4m3_encode(float x) {
+  const uint8_t sgn = std::signbit(x) ? 0x80 : 0;
+  const float a = std::fabs(x);
+  if (a >= 448.f) return sgn | 0x7E;
+  if (a < 0.015625f) return sgn | (uint8_t)std::nearbyint(a * 512.f);  // 8 is the code of 2^-6
+  int e;
+  (void)std::frexp(a, &e);
+  e -= 1;  // a in [2^e, 2^(e + 1))
+  int m = (int)std::nearbyint(std::ldexp(a, -e) * 8.f) - 8;  // 0..8 (8: carry into the exponent)
+  if (m == 8) {
+    e += 1;
+    m = 0;
+  }
+  return sgn | (uint8_t)(((e + 7) << 3) | m);
+}
+
+// Per-row E4M3 quantisation (the rule documented at fd_quantize_e4m3_rows).
+bool quantize_rows_e4m3(const float* in, int64_t rows, int64_t cols, uint8_t* codes, float* scales) {
+  for (int64_t r = 0; r < rows; ++r) {
+    const float* x = in + r * cols;
+    float m = 0.f;
+    for (int64_t c = 0; c < cols; ++c) {
+      if (!std::isfinite(x[c])) return false;
+      m = std::max(m, std::fabs(x[c]));
+    }
+    const float mm = m > 0.f ? m : 448.f;
+    const float inv = 448.f / mm;
+    for (int64_t c = 0; c < cols; ++c)
+      codes[r * cols + c] = e4m3_encode(std::fmin(448.f, std::fmax(-448.f, x[c] * inv)));
+    scales[r] = mm / 448.f;
+  }
+  return true;
+}
 
 }  // namespace
 
@@ -235,6 +279,8 @@ struct fd_kv_cache {
   void* ws = nullptr;
   float *x_bb = nullptr, *x_rf = nullptr, *raw = nullptr;
   void *a = nullptr, *q = nullptr, *o = nullptr, *h = nullptr, *u = nullptr;
+  uint8_t *a8 = nullptr, *h8 = nullptr;  // E4M3 MLP operands (FP8 MLP)
+  float *sa = nullptr, *sh = nullptr;     // their per-row scales
   float2* rope_t = nullptr;  // temporal RoPE (cos, sin) of the current call
   Probe probe;
 };
@@ -304,15 +350,30 @@ fd::GemmArgs gemm_args(const void* A, int lda, const void* W, int M, int N, int 
   return g;
 }
 
-fd_status run_norm(Ctx& x, const float* src, int M, const float* g, const float* b) {
+// Norm into the operand buffer a (compute type), or, for the FP8 MLP input,
+// into E4M3 codes a8 with per-row scales sa.
+fd_status run_norm(Ctx& x, const float* src, int M, const float* g, const float* b, bool e4m3 = false) {
   const fd_decoder* dec = x.dec;
   hipEvent_t ev;
   fd_status st = probe_begin(x.c, FD_KC_NORM, x.s, &ev);
   if (st) return st;
-  hipError_t e = fd::norm_rows(src, M, dec->cfg.dim, g, b, dec->cfg.norm_kind, dec->cfg.norm_eps,
-                               x.c->a, dec->d.act_kind, x.s);
+  hipError_t e = e4m3 ? fd::norm_rows(src, M, dec->cfg.dim, g, b, dec->cfg.norm_kind, dec->cfg.norm_eps,
+                                      x.c->a8, 3, x.s, x.c->sa)
+                      : fd::norm_rows(src, M, dec->cfg.dim, g, b, dec->cfg.norm_kind, dec->cfg.norm_eps,
+                                      x.c->a, dec->d.act_kind, x.s);
   if (e != hipSuccess) return fail(FD_ERR_DEVICE, "norm launch failed: %s", hipGetErrorString(e));
-  return probe_end(x.c, x.s, ev, (double)M * dec->cfg.dim * (4.0 + dec->d.act_bytes));
+  return probe_end(x.c, x.s, ev, (double)M * dec->cfg.dim * (4.0 + (e4m3 ? 1.0 : dec->d.act_bytes)));
+}
+
+fd_status run_gemm8(Ctx& x, const fd::GemmArgs& g, double algo_k) {
+  hipEvent_t ev;
+  fd_status st = probe_begin(x.c, FD_KC_GEMM, x.s, &ev);
+  if (st) return st;
+  hipError_t e = fd::gemm_fp8(g, x.s);
+  if (e != hipSuccess)
+    return fail(FD_ERR_DEVICE, "fp8 gemm launch (M=%d N=%d K=%d epi=%d) failed: %s", g.M, g.N, g.K,
+                (int)g.epi, hipGetErrorString(e));
+  return probe_end(x.c, x.s, ev, 2.0 * g.M * (double)g.N * algo_k);
 }
 
 fd_status trace_copy(Ctx& x, const float* src, int64_t n) {
@@ -420,6 +481,29 @@ fd_status run_stack(Ctx& x, const std::vector<LayerW>& layers, float* xs, int ro
     g.ep.ld_out = D;
     if ((st = run_gemm(x, g, D))) return st;
 
+    if (d.mlp8) {
+      // FP8 MLP (Sec. 4.6 "-Opt"): E4M3 MLP input per token, w13 with the fused
+      // SwiGLU into fp16, per-token E4M3 codes of that, w2 with the residual add
+      if ((st = run_norm(x, xs, rows, w.n2g, w.n2b, true))) return st;
+      g = gemm_args(kc->a8, D, w.w1, rows, 2 * H, D, fd::EPI_SWIGLU, w.b1);
+      g.ep.out_a = kc->h;
+      g.ep.ld_out = H;
+      g.ep.row_scale = kc->sa;
+      g.ep.col_scale = w.s1;
+      if ((st = run_gemm8(x, g, D))) return st;
+      if ((st = probe_begin(kc, FD_KC_NORM, x.s, &ev))) return st;
+      e = fd::quant_rows_e4m3(kc->h, 0, rows, H, kc->h8, kc->sh, x.s);
+      if (e != hipSuccess) return fail(FD_ERR_DEVICE, "quantisation launch failed: %s", hipGetErrorString(e));
+      if ((st = probe_end(kc, x.s, ev, (double)rows * H * 3.0))) return st;
+      g = gemm_args(kc->h8, H, w.w2, rows, D, H, fd::EPI_RESID_ADD, w.b2);
+      g.ep.out_f = xs;
+      g.ep.ld_out = D;
+      g.ep.row_scale = kc->sh;
+      g.ep.col_scale = w.s2;
+      if ((st = run_gemm8(x, g, H))) return st;
+      if ((st = trace_copy(x, xs, (int64_t)rows * D))) return st;
+      continue;
+    }
     if ((st = run_norm(x, xs, rows, w.n2g, w.n2b))) return st;
     if (c.mlp_kind == FD_MLP_SWIGLU) {
       if (d.is16) {
@@ -559,10 +643,19 @@ fd_status upload_weights(fd_decoder* dec, const void* w, int32_t wdt, size_t n_e
     const int64_t rows = d.is16 ? (t.s0 + 15) / 16 * 16 : t.s0;
     return (size_t)rows * mat_k(t);
   };
+  auto ends_with = [](const std::string& n, const char* suf) {
+    const size_t k = std::strlen(suf);
+    return n.size() > k && n.compare(n.size() - k, k, suf) == 0;
+  };
+  // FP8 MLP: w13 and w2 are stored as E4M3 codes (1 byte) plus per-row scales
+  auto is_fp8 = [&](const TensorSpec& t) {
+    return d.mlp8 && t.ndim == 2 && (ends_with(t.name, ".w13") || ends_with(t.name, ".w2"));
+  };
   size_t wbytes = 0, fbytes = 0;
   for (auto& t : specs) {
-    if (t.ndim == 2) wbytes += (mat_elems(t) * d.act_bytes + 255) / 256 * 256;
+    if (t.ndim == 2) wbytes += (mat_elems(t) * (is_fp8(t) ? 1 : d.act_bytes) + 255) / 256 * 256;
     else fbytes += ((size_t)t.s0 * 4 + 255) / 256 * 256;
+    if (is_fp8(t)) fbytes += ((size_t)t.s0 * 4 + 255) / 256 * 256;
   }
   if (hipMalloc(&dec->wmem, wbytes) != hipSuccess)
     return fail(FD_ERR_OUT_OF_MEMORY, "weights: hipMalloc(%zu) failed", wbytes);
@@ -606,7 +699,28 @@ fd_status upload_weights(fd_decoder* dec, const void* w, int32_t wdt, size_t n_e
     };
     if (swiglu_pack && (is_w13 || is_b13)) src = interleave(src, is_w13 ? t.s1 : 1);
     const void* dptr;
-    if (t.ndim == 2) {
+    const float* wscale = nullptr;
+    if (is_fp8(t)) {  // per-row E4M3 codes, packed in 16-row x 64-byte blocks
+      const int64_t K = t.s1, rows16 = (t.s0 + 15) / 16 * 16;
+      std::vector<uint8_t> codes((size_t)t.s0 * K), packed((size_t)rows16 * K, 0);
+      std::vector<float> scales(t.s0);
+      if (!quantize_rows_e4m3(src.data(), t.s0, K, codes.data(), scales.data())) {
+        st = fail(FD_ERR_INVALID_ARGUMENT, "weight %s has a non-finite value", t.name.c_str());
+        break;
+      }
+      for (int64_t r = 0; r < t.s0; ++r)
+        for (int64_t k = 0; k < K; k += 64)
+          std::memcpy(&packed[fd::pack_w8_index(r, k, K)], &codes[r * K + k], 64);
+      if (hipMemcpy(wp, packed.data(), packed.size(), hipMemcpyHostToDevice) != hipSuccess ||
+          hipMemcpy(fp, scales.data(), scales.size() * 4, hipMemcpyHostToDevice) != hipSuccess) {
+        st = fail(FD_ERR_DEVICE, "weight upload of %s failed", t.name.c_str());
+        break;
+      }
+      dptr = wp;
+      wscale = (const float*)fp;
+      wp += (packed.size() + 255) / 256 * 256;
+      fp += (scales.size() * 4 + 255) / 256 * 256;
+    } else if (t.ndim == 2) {
       size_t elems = mat_elems(t);
       if (t.name == "embed.w" && d.K_pad != t.s1) {
         host.assign((size_t)t.s0 * d.K_pad, 0.f);
@@ -676,9 +790,14 @@ fd_status upload_weights(fd_decoder* dec, const void* w, int32_t wdt, size_t n_e
       else if (f2 == "bo") L.bo = f;
       else if (f2 == "norm2.g") L.n2g = f;
       else if (f2 == "norm2.b") L.n2b = f;
-      else if (f2 == "w13" || f2 == "w1") L.w1 = dptr;
-      else if (f2 == "b13" || f2 == "b1") L.b1 = f;
-      else if (f2 == "w2") L.w2 = dptr;
+      else if (f2 == "w13" || f2 == "w1") {
+        L.w1 = dptr;
+        L.s1 = wscale;
+      } else if (f2 == "b13" || f2 == "b1") L.b1 = f;
+      else if (f2 == "w2") {
+        L.w2 = dptr;
+        L.s2 = wscale;
+      }
       else if (f2 == "b2") L.b2 = f;
     }
   }
@@ -870,7 +989,10 @@ fd_status fd_kv_cache_create(const fd_decoder* dec, int32_t batch, fd_kv_cache**
   const size_t sz_a = al(MR * D * es), sz_q = sz_a, sz_o = sz_a;
   const size_t sz_h = al(MR * hid * es), sz_u = al(M * d.K_pad * es);
   const size_t sz_rt = al((int64_t)c.max_frames_per_call * c.r_t * (d.Dh / 2) * sizeof(float2));
-  const size_t ws = sz_xbb + sz_xrf + sz_raw + sz_a + sz_q + sz_o + sz_h + sz_u + sz_rt;
+  const size_t sz_a8 = d.mlp8 ? al(MR * D) : 0, sz_h8 = d.mlp8 ? al(MR * c.mlp_hidden) : 0;
+  const size_t sz_sc = d.mlp8 ? al(MR * 4) : 0;
+  const size_t ws = sz_xbb + sz_xrf + sz_raw + sz_a + sz_q + sz_o + sz_h + sz_u + sz_rt + sz_a8 + sz_h8 +
+                    2 * sz_sc;
   if (hipMalloc(&kc->ws, ws) != hipSuccess) {
     free_cache(kc);
     return fail(FD_ERR_OUT_OF_MEMORY, "workspace: hipMalloc(%zu) failed", ws);
@@ -885,6 +1007,12 @@ fd_status fd_kv_cache_create(const fd_decoder* dec, int32_t batch, fd_kv_cache**
   kc->h = p; p += sz_h;
   kc->u = p; p += sz_u;
   kc->rope_t = (float2*)p; p += sz_rt;
+  if (d.mlp8) {
+    kc->a8 = (uint8_t*)p; p += sz_a8;
+    kc->h8 = (uint8_t*)p; p += sz_h8;
+    kc->sa = (float*)p; p += sz_sc;
+    kc->sh = (float*)p; p += sz_sc;
+  }
   *out = kc;
   return FD_OK;
 }
@@ -1033,6 +1161,75 @@ fd_status fd_measure_mfma_peak(int32_t dtype, int32_t iters, void* stream, doubl
   }
   *tflops = (double)blocks * 4.0 * iters * 16.0 * 32768.0 / (ms * 1e-3) / 1e12;
   *clock_ghz = ticks > 0 ? cyc / ticks * wclk_khz * 1e-6 : 0.0;
+  return FD_OK;
+}
+
+fd_status fd_quantize_e4m3_rows(const float* in, int64_t rows, int64_t cols, uint8_t* codes,
+                                float* scales) {
+  if (rows < 0 || cols < 1) return fail(FD_ERR_INVALID_ARGUMENT, "rows >= 0 and cols >= 1 required");
+  if (rows > 0 && (!in || !codes || !scales)) return fail(FD_ERR_INVALID_ARGUMENT, "NULL pointer");
+  if (!quantize_rows_e4m3(in, rows, cols, codes, scales))
+    return fail(FD_ERR_INVALID_ARGUMENT, "non-finite input");
+  return FD_OK;
+}
+
+fd_status fd_quantize_e4m3_rows_device(const float* in, int64_t rows, int64_t cols, uint8_t* codes,
+                                       float* scales, void* stream) {
+  if (rows < 0 || cols < 8 || cols > 65536 || cols % 8)
+    return fail(FD_ERR_INVALID_ARGUMENT, "cols must be a multiple of 8 in [8, 65536], rows >= 0");
+  if (rows > 0 && (!in || !codes || !scales)) return fail(FD_ERR_INVALID_ARGUMENT, "NULL pointer");
+  hipError_t e = fd::quant_rows_e4m3(in, 2, rows, (int)cols, codes, scales, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(FD_ERR_DEVICE, "quantisation launch failed: %s", hipGetErrorString(e));
+  return FD_OK;
+}
+
+fd_status fd_pack_e4m3_weight(const uint8_t* w, int64_t n, int64_t k, uint8_t* packed) {
+  if (n < 1 || k < 64 || k % 64) return fail(FD_ERR_INVALID_ARGUMENT, "N >= 1 and K a positive multiple of 64 required");
+  if (!w || !packed) return fail(FD_ERR_INVALID_ARGUMENT, "NULL pointer");
+  const int64_t rows16 = (n + 15) / 16 * 16;
+  std::memset(packed, 0, (size_t)(rows16 * k));
+  for (int64_t r = 0; r < n; ++r)
+    for (int64_t c = 0; c < k; c += 64) std::memcpy(&packed[fd::pack_w8_index(r, c, k)], &w[r * k + c], 64);
+  return FD_OK;
+}
+
+fd_status fd_gemm_e4m3_device(const uint8_t* a, int64_t lda, const float* a_scale,
+                              const uint8_t* w_packed, const float* w_scale, const float* bias,
+                              int32_t m, int32_t n, int32_t k, int32_t epilogue, void* out,
+                              int64_t ld_out, void* stream) {
+  if (m < 0 || n < 1 || k < 64 || k > 65536 || k % 64)
+    return fail(FD_ERR_INVALID_ARGUMENT, "M >= 0, N >= 1 and K a multiple of 64 in [64, 65536] required");
+  if (lda < k || lda % 16 || lda >= (1 << 20) || ld_out >= (1 << 20))
+    return fail(FD_ERR_INVALID_ARGUMENT, "lda must be a multiple of 16 in [K, 2^20), ld_out below 2^20");
+  if (epilogue != FD_GEMM_E4M3_RESID_ADD && epilogue != FD_GEMM_E4M3_SWIGLU_F16)
+    return fail(FD_ERR_INVALID_ARGUMENT, "unknown epilogue %d", epilogue);
+  const bool swiglu = epilogue == FD_GEMM_E4M3_SWIGLU_F16;
+  if (swiglu && (n % 64 || ld_out < n / 2 || ld_out % 4 || (uintptr_t)out % 8))
+    return fail(FD_ERR_INVALID_ARGUMENT,
+                "SwiGLU needs N % 64 == 0, ld_out >= N / 2 and a multiple of 4, out 8-byte aligned");
+  if (!swiglu && ld_out < n) return fail(FD_ERR_INVALID_ARGUMENT, "ld_out >= N required");
+  if (m == 0) return FD_OK;
+  if (!a || !a_scale || !w_packed || !w_scale || !bias || !out)
+    return fail(FD_ERR_INVALID_ARGUMENT, "NULL pointer");
+  if ((uintptr_t)a % 16 || (uintptr_t)w_packed % 16 || (!swiglu && (uintptr_t)out % 4))
+    return fail(FD_ERR_INVALID_ARGUMENT, "a and w_packed must be 16-byte aligned, out 4-byte aligned");
+  fd::GemmArgs g;
+  g.A = a;
+  g.W = w_packed;
+  g.M = m;
+  g.N = n;
+  g.K = k;
+  g.lda = (int)lda;
+  g.ldw = k;
+  g.epi = swiglu ? fd::EPI_SWIGLU : fd::EPI_RESID_ADD;
+  g.ep.bias = bias;
+  g.ep.row_scale = a_scale;
+  g.ep.col_scale = w_scale;
+  g.ep.ld_out = (int)ld_out;
+  if (swiglu) g.ep.out_a = out;
+  else g.ep.out_f = (float*)out;
+  hipError_t e = fd::gemm_fp8(g, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(FD_ERR_DEVICE, "E4M3 GEMM launch failed: %s", hipGetErrorString(e));
   return FD_OK;
 }
 

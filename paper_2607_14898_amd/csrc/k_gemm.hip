@@ -380,9 +380,12 @@ __device__ __forceinline__ void store_tile(const EpiParams& ep, const f32x16 (&a
 // 4 lk + 0..3. Every destination access covers those four columns at once (one
 // 16-byte fp32 or 8-byte 16-bit access) whenever the four land contiguously;
 // vec == false (a ragged or unaligned destination) stores element by element.
-template <int EPI, typename T, int FM, int FN>
+template <int EPI, typename T, int FM, int FN, bool SCALED = false>
 __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (&acc)[FM][FN], int r0,
                                              int c0, int M, int N, int lr, int lk, bool vec) {
+  // SCALED (FP8 GEMM, SwiGLU only): each accumulator is multiplied by its
+  // column's then its row's dequantisation scale right before use
+  static_assert(!SCALED || EPI == EPI_SWIGLU, "scaled transposed epilogue: SwiGLU only");
   typedef __attribute__((ext_vector_type(4))) float f4;
   int64_t ro[FM];
   bool rok[FM];
@@ -393,6 +396,9 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
     ro[i] = row_off<EPI>(ep, min(row, M - 1));
   }
   if constexpr (EPI == EPI_SWIGLU) {
+    float rs[FM];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) rs[i] = SCALED ? ep.row_scale[min(r0 + i * 32 + lr, M - 1)] : 1.f;
     // gate block j and up block j + 1 give output columns (c0 + 32 j) / 2 + 0..31
 #pragma unroll
     for (int j = 0; j < FN; j += 2)
@@ -400,11 +406,13 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
       for (int q = 0; q < 4; ++q) {
         const int lc = 8 * q + 4 * lk, pc = c0 + j * 32 + lc;
         if (pc >= N) continue;  // N % 64 == 0: a group is valid as a whole
-        float bg[4], bu[4];
+        float bg[4], bu[4], sg[4], su[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           bg[e] = ep.bias[pc + e];
           bu[e] = ep.bias[pc + 32 + e];
+          sg[e] = SCALED ? ep.col_scale[pc + e] : 1.f;
+          su[e] = SCALED ? ep.col_scale[pc + 32 + e] : 1.f;
         }
         const int oc = (c0 + j * 32) / 2 + lc;
 #pragma unroll
@@ -412,8 +420,14 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
           if (!rok[i]) continue;
           T o4[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            o4[e] = to_act<T>(silu_f(acc[i][j][4 * q + e] + bg[e]) * (acc[i][j + 1][4 * q + e] + bu[e]));
+          for (int e = 0; e < 4; ++e) {
+            float g = acc[i][j][4 * q + e], u = acc[i][j + 1][4 * q + e];
+            if (SCALED) {
+              g = g * sg[e] * rs[i];
+              u = u * su[e] * rs[i];
+            }
+            o4[e] = to_act<T>(silu_f(g + bg[e]) * (u + bu[e]));
+          }
           *reinterpret_cast<uint2*>((T*)ep.out_a + ro[i] + oc) = *reinterpret_cast<const uint2*>(o4);
         }
       }
@@ -679,6 +693,197 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
                                                                    reinterpret_cast<float*>(lds));
 }
 
+// ---------------------------------------------------------------------------
+// E4M3 GEMM (the FP8 MLP of the "-Opt" decoder, Sec. 4.6) on the gfx950
+// 32x32x64 FP8 MFMA. The memory path is that of the 16-bit kernel: a 64-byte
+// stage row now holds 64 K-values, one MFMA k-step, whose fragment (32
+// consecutive K-values of one row per lane, K-half lk) is two 16-byte chunks
+// of the swizzled stage row. Fragments are double-buffered across tiles: tile
+// t + 1's are read while tile t's MFMAs run. Before the epilogue the
+// accumulator of (m, n) is multiplied by row_scale[m] col_scale[n] (the
+// per-token activation and per-channel weight scales).
+// ---------------------------------------------------------------------------
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ f32x16 mfma_e4m3(i32x8 a, i32x8 b, f32x16 c) {
+  // format fields 0 / 0: both operands OCP E4M3; no block scales
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+
+template <class C, int EPI>
+__global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_fp8_kernel(
+    const uint8_t* __restrict__ A, const uint8_t* __restrict__ W, int M, int N, int K, int lda,
+    EpiParams ep, int tiles_m, int tiles_n) {
+  constexpr int BM = C::BM, BN = C::BN, FM = C::FM, FN = C::FN, NS = C::NS, NW = C::NW;
+  constexpr int QA = C::QA, Q = C::QA + C::QB, STAGE = C::STAGE;
+  constexpr bool TR = kTransposed<EPI>;
+  __shared__ uint4 lds[NS * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int tm, tn;
+  tile_of(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int wm0 = (wave / C::WAVES_N) * C::WM, wn0 = (wave % C::WAVES_N) * C::WN;
+
+  const int KB = K / 64;  // K tiles (64-byte stage rows)
+  const __amdgpu_buffer_rsrc_t rA = make_rsrc(A + (int64_t)m0 * lda, (uint32_t)min(BM, M - m0) * (uint32_t)lda);
+  const int nrows_w = min(BN, (N + 15) / 16 * 16 - n0);
+  const __amdgpu_buffer_rsrc_t rB =
+      make_rsrc(W + (int64_t)(n0 / 16) * KB * 1024, (uint32_t)(nrows_w / 16) * KB * 1024u);
+  const int lrow = lane >> 2, lchunk = (lane & 3) ^ ((lane >> 4) & 3);
+  uint32_t voff[Q];
+#pragma unroll
+  for (int j = 0; j < Q; ++j) {
+    const int q = j * NW + wave;
+    voff[j] = j < QA ? (uint32_t)((16 * q + lrow) * lda + lchunk * 16)
+                     : (uint32_t)(q - BM / 16) * KB * 1024u + (uint32_t)(lrow * 64 + lchunk * 16);
+  }
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint4*)lds;
+  auto dma = [&](int st, int kt) {
+    const uint32_t soffA = (uint32_t)kt * 64u, soffB = (uint32_t)kt * 1024u;
+#pragma unroll
+    for (int j = 0; j < Q; ++j) {
+      const uint32_t m0addr = lds0 + (uint32_t)(st * STAGE + 64 * (j * NW + wave)) * 16u;
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+      asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                   :
+                   : "s"(m0addr), "v"(voff[j]), "s"(j < QA ? rA : rB), "s"(j < QA ? soffA : soffB)
+                   : "m0");
+#pragma clang diagnostic pop
+    }
+  };
+  auto sync = [&](bool drain) {
+    if (drain) __builtin_amdgcn_s_waitcnt(FD_VMCNT(0));
+    else __builtin_amdgcn_s_waitcnt(FD_VMCNT((NS - 2) * Q));
+    __builtin_amdgcn_s_waitcnt(FD_LGKMCNT0);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int lr = lane & 31, lk = lane >> 5, xr = (lr >> 2) & 3;
+  // the two chunks of fragment row (A: wm0 + lr, W: BM + wn0 + lr): K-chunks 2 lk, 2 lk + 1
+  const int ia0 = (wm0 + lr) * 4 + ((2 * lk) ^ xr), ia1 = (wm0 + lr) * 4 + ((2 * lk + 1) ^ xr);
+  const int ib0 = (BM + wn0 + lr) * 4 + ((2 * lk) ^ xr), ib1 = (BM + wn0 + lr) * 4 + ((2 * lk + 1) ^ xr);
+  // 8-wave tiles leave 256 registers per lane: double-buffering both operands'
+  // fragments (96) beside 128 accumulators would spill, so the W fragments are
+  // single-buffered there and each W block is re-read for the next tile as
+  // soon as its last MFMA has issued.
+  constexpr bool FB1 = NW == 8;
+  i32x8 fa[2][FM], fb[FB1 ? 1 : 2][FN];
+  auto load_fa1 = [&](int slot, int st, int i) {
+    const uint4* sb = lds + st * STAGE;
+    const uint4 v0 = sb[ia0 + i * 128], v1 = sb[ia1 + i * 128];
+    fa[slot][i] = i32x8{(int)v0.x, (int)v0.y, (int)v0.z, (int)v0.w, (int)v1.x, (int)v1.y, (int)v1.z, (int)v1.w};
+  };
+  auto load_fa = [&](int slot, int st) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) load_fa1(slot, st, i);
+  };
+  auto load_fb = [&](int slot, int st, int j) {
+    const uint4* sb = lds + st * STAGE;
+    const uint4 v0 = sb[ib0 + j * 128], v1 = sb[ib1 + j * 128];
+    fb[slot][j] = i32x8{(int)v0.x, (int)v0.y, (int)v0.z, (int)v0.w, (int)v1.x, (int)v1.y, (int)v1.z, (int)v1.w};
+  };
+  // MFMAs of the tile in register slot `slot`; with FB1 and reload, W block j
+  // of the tile in stage next_st replaces block j once its MFMAs are issued
+  auto mfmas = [&](int slot, int next_st, bool reload) {
+    const int bs = FB1 ? 0 : slot;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        acc[i][j] = TR ? mfma_e4m3(fb[bs][j], fa[slot][i], acc[i][j]) : mfma_e4m3(fa[slot][i], fb[bs][j], acc[i][j]);
+      if (FB1 && reload) load_fb(0, next_st, j);
+    }
+  };
+
+  // Tile t sits in stage t % NS. Iteration t: the barrier publishes tile t + 1
+  // (and frees the stage read in iteration t - 1), its fragments are read
+  // into register slot (t + 1) & 1, the stage of tile t is refilled with tile
+  // t + NS, and tile t's MFMAs run from slot t & 1. The loop runs two
+  // iterations per trip so that both slots are compile-time indices (a
+  // run-time index would put the fragment arrays in scratch memory).
+  const int KT = KB;
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < KT) dma(p, p);
+  sync(KT < NS - 1);
+  load_fa(0, 0);
+#pragma unroll
+  for (int j = 0; j < FN; ++j) load_fb(0, 0, j);
+  if (NS - 1 < KT) dma(NS - 1, NS - 1);
+  int sc = 0;
+  auto step = [&](int t, int load_slot, int mfma_slot) {
+    const int sn = sc + 1 == NS ? 0 : sc + 1;
+    sync(t + NS - 1 >= KT);
+    load_fa(load_slot, sn);
+    if (!FB1) {
+#pragma unroll
+      for (int j = 0; j < FN; ++j) load_fb(load_slot, sn, j);
+    }
+    if (t + NS < KT) dma(sc, t + NS);
+    mfmas(mfma_slot, sn, true);
+    sc = sn;
+  };
+  int t = 0;
+  for (; t + 2 <= KT - 1; t += 2) {
+    step(t, 1, 0);
+    step(t + 1, 0, 1);
+  }
+  if (t < KT - 1) {
+    step(t, 1, 0);
+    ++t;
+  }
+  // t == KT - 1: the last tile's fragments move to slot 0 (a branch around the
+  // MFMAs instead would merge two copies of the accumulators and spill)
+  if (t & 1) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) fa[0][i] = fa[1][i];
+    if (!FB1) {
+#pragma unroll
+      for (int j = 0; j < FN; ++j) fb[0][j] = fb[FB1 ? 0 : 1][j];
+    }
+  }
+  mfmas(0, 0, false);
+
+  // dequantisation by column then row scale: inside the transposed SwiGLU store,
+  // per element; here, in the accumulator layout, for the residual add
+  const int r0 = m0 + wm0, c0 = n0 + wn0;
+  if constexpr (TR) {  // lane: row r0 + 32 i + lr; columns c0 + 32 j + 8 q + 4 lk + e
+    store_tile_t<EPI, _Float16, FM, FN, true>(ep, acc, r0, c0, M, N, lr, lk, true);
+  } else {  // lane: column c0 + 32 j + lr; rows r0 + 32 i + 8 (r / 4) + 4 lk + r % 4
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const float cs = ep.col_scale[min(c0 + j * 32 + lr, N - 1)];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] *= cs;
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float rs = ep.row_scale[min(r0 + i * 32 + 8 * (r >> 2) + 4 * lk + (r & 3), M - 1)];
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j][r] *= rs;
+      }
+    store_tile<EPI, _Float16, FM, FN, !(C::NW == 4 && C::MIN_BLOCKS == 1)>(ep, acc, r0, c0, M, N, lr, lk,
+                                                                          reinterpret_cast<float*>(lds));
+  }
+}
+
 template <typename T, class C, int EPI>
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   const int tm = (g.M + C::BM - 1) / C::BM, tn = (g.N + C::BN - 1) / C::BN;
@@ -793,7 +998,37 @@ hipError_t launch_f32(const GemmArgs& g, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <class C, int EPI>
+hipError_t launch_fp8(const GemmArgs& g, hipStream_t s) {
+  const int tm = (g.M + C::BM - 1) / C::BM, tn = (g.N + C::BN - 1) / C::BN;
+  hipLaunchKernelGGL((gemm_fp8_kernel<C, EPI>), dim3(tm * tn), dim3(C::NT), 0, s, (const uint8_t*)g.A,
+                     (const uint8_t*)g.W, g.M, g.N, g.K, g.lda, g.ep, tm, tn);
+  return hipGetLastError();
+}
+
+template <int EPI>
+hipError_t dispatch_fp8(const GemmArgs& g, hipStream_t s) {
+  auto tiles = [&](int bm, int bn) { return ((g.M + bm - 1) / bm) * ((g.N + bn - 1) / bn); };
+  // (256 x 256 tiles would spill the residual epilogue's registers)
+  if constexpr (EPI != EPI_RESID_ADD)
+    if (tiles(256, 256) >= 160) return launch_fp8<TileL, EPI>(g, s);
+  const int tm = tiles(192, 128);
+  if (tm >= 200) return launch_fp8<TileM, EPI>(g, s);
+  return launch_fp8<TileS, EPI>(g, s);
+}
+
 }  // namespace
+
+hipError_t gemm_fp8(const GemmArgs& g, hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  if (g.K <= 0 || g.K % 64 || g.lda % 16 || !g.ep.row_scale || !g.ep.col_scale) return hipErrorInvalidValue;
+  if (g.epi == EPI_SWIGLU) {
+    if (g.N % 64 || g.ep.ld_out % 4 || (uintptr_t)g.ep.out_a % 8) return hipErrorInvalidValue;
+    return dispatch_fp8<EPI_SWIGLU>(g, s);
+  }
+  if (g.epi == EPI_RESID_ADD) return dispatch_fp8<EPI_RESID_ADD>(g, s);
+  return hipErrorInvalidValue;
+}
 
 hipError_t gemm_mfma(Act16 t, const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;

@@ -7,7 +7,8 @@
 //                    (unit mod S);
 //  * unshuffle_latent PixelUnshuffle(p) + raster flatten of latent frames
 //                    (Sec. 4.3 and Eq. projection);
-//  * swiglu_f32      SwiGLU gate of the fp32 path.
+//  * swiglu_f32      SwiGLU gate of the fp32 path;
+//  * quant_rows_e4m3 per-row E4M3 codes and scales of the FP8 MLP (Sec. 4.6).
 #include "fd_kernels.h"
 
 #include <hip/hip_bf16.h>
@@ -42,12 +43,38 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+// E4M3 quantisation of a row whose amplitude (max |v|) is m: inv = 448 / m,
+// codes of fp32(v * inv) by the gfx950 conversion (round to nearest even),
+// after clamping to +-448 so that the code saturates; scale m / 448. A zero
+// row gets scale 1 (and codes 0).
+struct E4m3Row {
+  float inv, scale;
+  __device__ __forceinline__ explicit E4m3Row(float m) {
+    const float mm = m > 0.f ? m : 448.f;
+    inv = 448.f / mm;
+    scale = mm / 448.f;
+  }
+  // four values -> four codes, byte e = value e
+  __device__ __forceinline__ uint32_t pack4(float a, float b, float c, float d) const {
+    auto cl = [&](float v) { return fminf(448.f, fmaxf(-448.f, v * inv)); };
+    int w = __builtin_amdgcn_cvt_pk_fp8_f32(cl(a), cl(b), 0, false);
+    w = __builtin_amdgcn_cvt_pk_fp8_f32(cl(c), cl(d), w, true);
+    return (uint32_t)w;
+  }
+};
+
 // One wave per row; rows of D floats (D % 4 == 0).
 template <int KIND>
 __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, int M, int D,
                                                    const float* __restrict__ g,
                                                    const float* __restrict__ bta, float eps,
-                                                   void* out, int out_kind) {
+                                                   void* out, int out_kind, float* row_scale) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
@@ -83,6 +110,7 @@ __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, 
     q = wave_sum(q);
     rs = rsqrtf(q / D + eps);
   }
+  float amax = 0.f;
 #pragma unroll
   for (int i = 0; i < MAXV; ++i) {
     const int c = lane + 64 * i;
@@ -94,9 +122,52 @@ __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, 
         const float4 bv = reinterpret_cast<const float4*>(bta)[c];
         y.x += bv.x; y.y += bv.y; y.z += bv.z; y.w += bv.w;
       }
-      store4(out, (int64_t)row * D + 4 * c, y, out_kind);
+      if (out_kind == 3) {  // E4M3: keep the row for its amplitude
+        v[i] = y;
+        amax = fmaxf(fmaxf(amax, fmaxf(fabsf(y.x), fabsf(y.y))), fmaxf(fabsf(y.z), fabsf(y.w)));
+      } else {
+        store4(out, (int64_t)row * D + 4 * c, y, out_kind);
+      }
     }
   }
+  if (out_kind == 3) {
+    const E4m3Row q(wave_max(amax));
+#pragma unroll
+    for (int i = 0; i < MAXV; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nv)
+        reinterpret_cast<uint32_t*>((uint8_t*)out + (int64_t)row * D)[c] = q.pack4(v[i].x, v[i].y, v[i].z, v[i].w);
+    }
+    if (lane == 0) row_scale[row] = q.scale;
+  }
+}
+
+// Per-row E4M3 codes of in [M, K] (fp16 or fp32, K % 8 == 0): one wave per row,
+// a first pass for the amplitude, a second (from cache) for the codes.
+template <typename TIN>
+__global__ __launch_bounds__(256) void quant_rows_kernel(const TIN* __restrict__ in, int64_t M, int K,
+                                                         uint8_t* __restrict__ codes,
+                                                         float* __restrict__ scale) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;
+  const TIN* r = in + row * K;
+  float amax = 0.f;
+  for (int c = 8 * lane; c < K; c += 512) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)r[c + e]));
+  }
+  const E4m3Row q(wave_max(amax));
+  for (int c = 8 * lane; c < K; c += 512) {
+    float f[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) f[e] = (float)r[c + e];
+    uint2 w;
+    w.x = q.pack4(f[0], f[1], f[2], f[3]);
+    w.y = q.pack4(f[4], f[5], f[6], f[7]);
+    *reinterpret_cast<uint2*>(codes + row * K + c) = w;
+  }
+  if (lane == 0) scale[row] = q.scale;
 }
 
 // cos / sin of the RoPE angle of channel pair `pair` for the row (frame-or-
@@ -261,14 +332,30 @@ int grid_for(int64_t total) {
 }  // namespace
 
 hipError_t norm_rows(const float* x, int M, int D, const float* g, const float* b, int kind,
-                     float eps, void* out, int out_kind, hipStream_t s) {
+                     float eps, void* out, int out_kind, hipStream_t s, float* row_scale) {
   if (M <= 0) return hipSuccess;
-  if (D % 4 || D > 2048) return hipErrorInvalidValue;
+  if (D % 4 || D > 2048 || (out_kind == 3 && !row_scale)) return hipErrorInvalidValue;
   const int grid = (M + 3) / 4;
   if (kind == 0)
-    hipLaunchKernelGGL(norm_kernel<0>, dim3(grid), dim3(256), 0, s, x, M, D, g, b, eps, out, out_kind);
+    hipLaunchKernelGGL(norm_kernel<0>, dim3(grid), dim3(256), 0, s, x, M, D, g, b, eps, out, out_kind,
+                       row_scale);
   else
-    hipLaunchKernelGGL(norm_kernel<1>, dim3(grid), dim3(256), 0, s, x, M, D, g, b, eps, out, out_kind);
+    hipLaunchKernelGGL(norm_kernel<1>, dim3(grid), dim3(256), 0, s, x, M, D, g, b, eps, out, out_kind,
+                       row_scale);
+  return hipGetLastError();
+}
+
+hipError_t quant_rows_e4m3(const void* in, int in_kind, int64_t M, int K, uint8_t* codes,
+                           float* scale, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (K <= 0 || K % 8 || (in_kind != 0 && in_kind != 2)) return hipErrorInvalidValue;
+  const unsigned grid = (unsigned)((M + 3) / 4);
+  if (in_kind == 0)
+    hipLaunchKernelGGL(quant_rows_kernel<_Float16>, dim3(grid), dim3(256), 0, s, (const _Float16*)in, M,
+                       K, codes, scale);
+  else
+    hipLaunchKernelGGL(quant_rows_kernel<float>, dim3(grid), dim3(256), 0, s, (const float*)in, M, K,
+                       codes, scale);
   return hipGetLastError();
 }
 

@@ -36,7 +36,8 @@ class fd_config(ctypes.Structure):
         ("rope_theta", ctypes.c_float), ("norm_eps", ctypes.c_float), ("r_t", ctypes.c_int32),
         ("s_out", ctypes.c_int32), ("out_channels", ctypes.c_int32), ("window", ctypes.c_int32),
         ("unit_frames", ctypes.c_int32), ("max_batch", ctypes.c_int32),
-        ("max_frames_per_call", ctypes.c_int32), ("clamp_output", ctypes.c_int32)]]
+        ("max_frames_per_call", ctypes.c_int32), ("clamp_output", ctypes.c_int32),
+        ("mlp_precision", ctypes.c_int32)]]
 
 
 class fd_tensor_desc(ctypes.Structure):
@@ -85,6 +86,10 @@ def load_library() -> ctypes.CDLL:
                                 ctypes.POINTER(ctypes.c_double)]),
         "fd_measure_mfma_peak": (I32, [I32, I32, P, ctypes.POINTER(ctypes.c_double),
                                        ctypes.POINTER(ctypes.c_double)]),
+        "fd_quantize_e4m3_rows": (I32, [P, I64, I64, P, P]),
+        "fd_quantize_e4m3_rows_device": (I32, [P, I64, I64, P, P, P]),
+        "fd_pack_e4m3_weight": (I32, [P, I64, I64, P]),
+        "fd_gemm_e4m3_device": (I32, [P, I64, P, P, P, P, I32, I32, I32, I32, P, I64, P]),
         "fd_status_string": (ctypes.c_char_p, [I32]),
         "fd_last_error": (ctypes.c_char_p, []),
     }
@@ -119,6 +124,7 @@ def make_config(model, max_batch: int = 1, max_frames_per_call: int = 4) -> fd_c
     c.rope_theta = float(model.rope_theta)
     c.norm_eps = float(model.norm_eps)
     c.clamp_output = int(model.clamp_output)
+    c.mlp_precision = {"f16": 0, "fp8": 1}[getattr(model, "mlp_precision", "f16")]
     c.max_batch = max_batch
     c.max_frames_per_call = max_frames_per_call
     return c
@@ -237,6 +243,49 @@ def fd_measure_mfma_peak(dtype: str = "f16", iters: int = 100000, stream=None):
     _check(load_library().fd_measure_mfma_peak(_DTYPES[dtype], iters, _stream_handle(stream),
                                                 ctypes.byref(tf), ctypes.byref(ghz)))
     return tf.value, ghz.value
+
+
+def fd_quantize_e4m3_rows(x: np.ndarray):
+    """Host E4M3 row quantisation (the FP8 MLP's weight rule): (codes uint8, scales fp32)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    rows, cols = x.shape
+    codes = np.empty((rows, cols), np.uint8)
+    scales = np.empty(rows, np.float32)
+    _check(load_library().fd_quantize_e4m3_rows(x.ctypes.data, rows, cols, codes.ctypes.data,
+                                                 scales.ctypes.data))
+    return codes, scales
+
+
+def fd_quantize_e4m3_rows_device(x, codes, scales, stream=None) -> None:
+    """Device E4M3 row quantisation of the fp32 torch tensor x [rows, cols] into
+    codes (uint8) and scales (fp32) torch tensors on the same GPU."""
+    rows, cols = x.shape
+    _check(load_library().fd_quantize_e4m3_rows_device(x.data_ptr(), rows, cols, codes.data_ptr(),
+                                                        scales.data_ptr(), _stream_handle(stream)))
+
+
+FD_GEMM_E4M3_RESID_ADD, FD_GEMM_E4M3_SWIGLU_F16 = 0, 1
+
+
+def fd_pack_e4m3_weight(w: np.ndarray) -> np.ndarray:
+    """Packed layout of an [N, K] uint8 E4M3 weight for fd_gemm_e4m3_device
+    (ceil(N / 16) * 16 * K bytes)."""
+    w = np.ascontiguousarray(w, dtype=np.uint8)
+    n, k = w.shape
+    out = np.empty(((n + 15) // 16 * 16) * k, np.uint8)
+    _check(load_library().fd_pack_e4m3_weight(w.ctypes.data, n, k, out.ctypes.data))
+    return out
+
+
+def fd_gemm_e4m3_device(a, a_scale, w_packed, w_scale, bias, n: int, k: int, epilogue: int,
+                        out, stream=None) -> None:
+    """E4M3 GEMM on torch device tensors: a [M, lda] uint8 codes, a_scale [M],
+    w_packed (fd_pack_e4m3_weight's bytes on the device), w_scale [N], bias
+    [N] fp32, out [M, ld_out] (fp32 residual, or fp16 for the SwiGLU epilogue)."""
+    m, lda = a.shape
+    _check(load_library().fd_gemm_e4m3_device(
+        a.data_ptr(), lda, a_scale.data_ptr(), w_packed.data_ptr(), w_scale.data_ptr(),
+        bias.data_ptr(), m, n, k, epilogue, out.data_ptr(), out.stride(0), _stream_handle(stream)))
 
 
 class Decoder:

@@ -2,6 +2,8 @@
 every function include/flashdecoder.h declares, validates configs, reports the
 canonical weight layout, and rejects bad arguments before touching a GPU."""
 import ctypes
+
+import numpy as np
 import os
 import re
 from dataclasses import replace
@@ -40,8 +42,8 @@ def test_library_exports_every_declared_function():
 
 def test_config_struct_size_matches_header():
     _lib()
-    # 1 uint32 + 27 int32/float fields, no padding
-    assert ctypes.sizeof(fdb.fd_config) == 4 * 28
+    # 1 uint32 + 28 int32/float fields, no padding
+    assert ctypes.sizeof(fdb.fd_config) == 4 * 29
 
 
 @pytest.mark.parametrize("name", list(MODELS))
@@ -69,6 +71,7 @@ def test_weight_layout_matches_generator(name):
     (dict(latent_h=61), fdb.FD_ERR_INVALID_ARGUMENT),      # H' % p != 0
     (dict(window=0), fdb.FD_ERR_INVALID_ARGUMENT),
     (dict(n_heads=48), fdb.FD_ERR_UNSUPPORTED),            # 16-bit path needs D_h = 64
+    (dict(mlp_precision="fp8", compute_dtype="f32"), fdb.FD_ERR_UNSUPPORTED),  # FP8 MLP needs 16-bit compute
 ])
 def test_invalid_configs_are_rejected(change, status):
     _lib()
@@ -117,3 +120,79 @@ def test_pack_weights_rejects_wrong_shapes():
     w["embed.w"] = np.zeros((3, 3), np.float32)
     with pytest.raises(ValueError):
         fdb.pack_weights(cfg, w)
+
+
+def _e4m3_decode(codes):
+    """Value of OCP E4M3 codes from the bit fields (sign, exponent bias 7, 3-bit mantissa)."""
+    c = codes.astype(np.int64)
+    sgn = np.where(c & 0x80, -1.0, 1.0)
+    e, m = (c >> 3) & 0xF, c & 7
+    mag = np.where(e == 0, m / 8.0 * 2.0 ** -6, (1 + m / 8.0) * 2.0 ** (e - 7))
+    return sgn * mag
+
+
+def test_host_e4m3_quantiser_matches_the_oracle_bit_for_bit():
+    """The library's weight quantiser (C++, used at create) against the
+    oracle's rule: same codes and scales, including exact midpoints, tiny,
+    saturating and zero rows."""
+    _lib()
+    from oracle.decoder import quant_rows_e4m3, e4m3_round
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal((12, 200)).astype(np.float32) * np.float32(0.02)
+    x[1] *= 1e-4
+    x[2] *= 1e4
+    x[3] = 0.0
+    # a row whose maximum is 448 (scale 1): exact midpoints between codes survive the scaling
+    mids = (np.unique(np.abs(e4m3_round(np.linspace(0, 448, 4000))))[1:] +
+            np.unique(np.abs(e4m3_round(np.linspace(0, 448, 4000))))[:-1]) / 2
+    x[4, :len(mids[:199])] = mids[:199].astype(np.float32)
+    x[4, 199] = 448.0
+    x[5, :100] = -x[4, :100]
+    x[5, 199] = 448.0
+    codes, scales = fdb.fd_quantize_e4m3_rows(x)
+    ref_q, ref_s = quant_rows_e4m3(x)
+    assert np.array_equal(scales.astype(np.float64), ref_s)
+    assert np.array_equal(_e4m3_decode(codes), ref_q)
+    assert np.all((codes & 0x7F) != 0x7F)                 # never the NaN code
+    with pytest.raises(fdb.FlashDecoderError):
+        fdb.fd_quantize_e4m3_rows(np.array([[1.0, np.nan]], np.float32))
+
+
+def test_e4m3_weight_packing_layout():
+    """fd_pack_e4m3_weight: 1 KB blocks of 16 rows x 64 K-columns, block-row
+    major, rows padded with zeros to a multiple of 16 (checked element by
+    element against the layout rule written out here)."""
+    _lib()
+    rng = np.random.default_rng(4)
+    N, K = 37, 192
+    w = rng.integers(0, 256, (N, K), dtype=np.uint8)
+    p = fdb.fd_pack_e4m3_weight(w)
+    assert p.size == 48 * K
+    want = np.zeros(48 * K, np.uint8)
+    for n in range(N):
+        for k in range(K):
+            blk = (n // 16) * (K // 64) + k // 64
+            want[blk * 1024 + (n % 16) * 64 + k % 64] = w[n, k]
+    assert np.array_equal(p, want)
+    lib = fdb.load_library()
+    buf = np.zeros(64 * 64, np.uint8)
+    assert lib.fd_pack_e4m3_weight(buf.ctypes.data, 4, 96, buf.ctypes.data) == fdb.FD_ERR_INVALID_ARGUMENT
+    assert lib.fd_pack_e4m3_weight(None, 4, 64, buf.ctypes.data) == fdb.FD_ERR_INVALID_ARGUMENT
+
+
+@pytest.mark.parametrize("m,n,k,lda,epi,ld_out", [
+    (4, 64, 96, 96, 0, 64),      # K not a multiple of 64
+    (4, 64, 64, 72, 0, 64),      # lda not a multiple of 16
+    (4, 64, 128, 64, 0, 64),     # lda < K
+    (4, 64, 64, 64, 0, 32),      # ld_out < N
+    (4, 96, 64, 64, 1, 48),      # SwiGLU with N % 64 != 0
+    (4, 128, 64, 64, 1, 62),     # SwiGLU ld_out not a multiple of 4
+    (4, 64, 64, 64, 2, 64),      # unknown epilogue
+    (-1, 64, 64, 64, 0, 64),
+    (4, 64, 64, 64, 0, 64),      # NULL pointers
+])
+def test_e4m3_gemm_rejects_bad_arguments_before_any_device_call(m, n, k, lda, epi, ld_out):
+    lib = _lib()
+    st = lib.fd_gemm_e4m3_device(None, lda, None, None, None, None, m, n, k, epi, None, ld_out, None)
+    assert st == fdb.FD_ERR_INVALID_ARGUMENT
+    assert lib.fd_last_error().decode() != ""

@@ -43,7 +43,7 @@ __all__ = [
     "pixel_shuffle_frame", "band_mask", "StreamingOracle", "decode_full",
     "decode_stream", "block_forward", "token_positions", "block_forward_rows",
     "stack_final", "temporal_up_rows", "head_rows", "e4m3_round", "quant_rows_e4m3",
-    "quant_weight_rows_e4m3", "e4m3_decode", "gemm_e4m3",
+    "quant_weight_rows_e4m3", "e4m3_decode", "gemm_e4m3", "pixels_to_u8", "pixels_to_bf16_bits",
 ]
 
 # --------------------------------------------------------------------------
@@ -143,6 +143,38 @@ def gemm_e4m3(a_codes: np.ndarray, a_scale: np.ndarray, w_codes: np.ndarray,
     acc = e4m3_decode(a_codes) @ e4m3_decode(w_codes).T
     return acc * np.asarray(a_scale, np.float64)[:, None] * \
         np.asarray(w_scale, np.float64)[None, :] + np.asarray(bias, np.float64)[None, :]
+
+
+# --------------------------------------------------------------------------
+# Output pixel formats (8-bit and bf16 RGB, the step after the fp32 output of
+# Sec. 3.4 Step 3)
+# --------------------------------------------------------------------------
+
+
+def pixels_to_u8(px: np.ndarray) -> np.ndarray:
+    """uint8 codes of fp32 pixels: rint(fp32(x * 127.5 + 127.5)) -- one fp32
+    rounding of the multiply-add, then the nearest integer, ties to even --
+    limited to 0..255 (-1 -> 0, 0 -> 128, 1 -> 255).
+
+    For fp32 |x| >= 2^-21 the sum is exact in fp64 (at most 53 significant
+    bits), so one conversion to fp32 is the single rounding. Below that the
+    fp32 result lies within a few steps of 127.5 (step 2^-17), and the code is
+    127 exactly when x * 127.5 < -2^-18 (the sum then rounds below 127.5; at
+    -2^-18 the tie goes to the even 127.5), else 128."""
+    x = np.asarray(px, dtype=np.float32).astype(np.float64)
+    v = (x * 127.5 + 127.5).astype(np.float32).astype(np.float64)
+    q = np.rint(v)
+    tiny = np.abs(x) < 2.0 ** -21
+    q = np.where(tiny, np.where(x * 127.5 < -2.0 ** -18, 127.0, 128.0), q)
+    return np.clip(q, 0, 255).astype(np.uint8)
+
+
+def pixels_to_bf16_bits(px: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns of fp32 pixels, rounded to nearest even: the top 16
+    bits of the fp32 pattern after adding 0x7FFF plus the lowest kept bit
+    (finite inputs)."""
+    b = np.asarray(px, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    return ((b + 0x7FFF + ((b >> 16) & 1)) >> 16).astype(np.uint16)
 
 
 # --------------------------------------------------------------------------

@@ -522,3 +522,60 @@ def test_e4m3_gemm_matches_a_scalar_loop_and_the_fake_quant_linear():
     cw = np.vectorize(inv.get)(qw).astype(np.uint8)
     bb = rng.standard_normal(7)
     np.testing.assert_allclose(gemm_e4m3(cx, sx, cw, sww, bb), _fp8_linear(x, wf, bb), rtol=0, atol=1e-12)
+
+
+# --------------------------------------------------------------------------
+# Output pixel formats
+# --------------------------------------------------------------------------
+
+def _fp32_round_exact(q):
+    """Nearest fp32 to the rational q, ties to the even significand, by search
+    around a first guess (independent of the oracle's formula)."""
+    from fractions import Fraction
+    c = np.float32(float(q))
+    best = None
+    for cand in (np.nextafter(c, np.float32(-np.inf)), c, np.nextafter(c, np.float32(np.inf))):
+        d = abs(Fraction(float(cand)) - q)
+        even = int(np.array(cand, np.float32).view(np.uint32)) % 2 == 0
+        key = (d, not even)
+        if best is None or key < best[0]:
+            best = (key, cand)
+    return best[1]
+
+
+def test_u8_pixels_equal_exact_rational_rounding():
+    """pixels_to_u8 against exact arithmetic: the rational x * 255/2 + 255/2,
+    rounded once to fp32 by search, then to the nearest integer (ties even)."""
+    from fractions import Fraction
+    from oracle.decoder import pixels_to_u8
+    rng = np.random.default_rng(21)
+    xs = np.concatenate([
+        rng.uniform(-1, 1, 3000), [-1.0, 1.0, 0.0, -0.0],
+        # values whose fp32 sum lands on or next to a .5 tie
+        (np.arange(-127, 129) - 0.5 - 127.5) / 127.5,
+        # tiny values around the 127 / 128 threshold x * 127.5 = -2^-18
+        -2.0 ** -18 / 127.5 * (1 + np.linspace(-1e-6, 1e-6, 41)),
+        rng.uniform(-1, 1, 200) * 2.0 ** -22, [2.0 ** -30, -2.0 ** -30, 1.5, -3.0]])
+    xs = xs.astype(np.float32)
+    got = pixels_to_u8(xs)
+    for x, g in zip(xs, got):
+        q = Fraction(float(x)) * Fraction(255, 2) + Fraction(255, 2)
+        v = Fraction(float(_fp32_round_exact(q)))
+        fl = v.numerator // v.denominator
+        frac = v - fl
+        r = fl + (1 if frac > Fraction(1, 2) or (frac == Fraction(1, 2) and fl % 2 == 1) else 0)
+        assert g == min(255, max(0, r)), (float(x), g, r)
+    assert list(pixels_to_u8(np.array([-1, 0, 1], np.float32))) == [0, 128, 255]
+
+
+def test_bf16_pixels_match_torch_rounding():
+    import torch
+    from oracle.decoder import pixels_to_bf16_bits
+    rng = np.random.default_rng(22)
+    x = np.concatenate([rng.uniform(-1, 1, 5000), rng.standard_normal(1000) * 1e-20,
+                        [0.0, -0.0, 1.0, -1.0]]).astype(np.float32)
+    # exact ties: patterns with the low 16 bits 0x8000
+    ties = (rng.integers(0x3C000000, 0x3F800000, 500, dtype=np.uint32) & 0xFFFF0000) | 0x8000
+    x = np.concatenate([x, ties.view(np.float32)])
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(pixels_to_bf16_bits(x), ref)

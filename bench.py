@@ -122,6 +122,10 @@ def main() -> int:
     ap.add_argument("--workload", default="xl-720p-stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, metavar="MIB")
+    ap.add_argument("--streams", type=int, default=1,
+                    help="independent streams decoded concurrently per step (fd_decode_chunks)")
+    ap.add_argument("--pixels", choices=["f32", "bf16", "u8"], default="f32",
+                    help="pixel format of the output store")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -142,20 +146,42 @@ def main() -> int:
     m = wl.model
     F = wl.frames_per_call
     weights = wl.weights()
+    fmt = {"f32": fdb.FD_PIXELS_F32, "bf16": fdb.FD_PIXELS_BF16, "u8": fdb.FD_PIXELS_U8}[args.pixels]
+    NS = args.streams
+    if NS < 1:
+        print("--streams must be >= 1", file=sys.stderr)
+        return 2
     dec = fdb.Decoder(m, weights, max_batch=1, max_frames_per_call=F)
-    cache = fdb.KvCache(dec, 1)
+    caches = [fdb.KvCache(dec, 1) for _ in range(NS)]
+    cache = caches[0]
     z = torch.from_numpy(wl.latents()).cuda()
     chunks = [z[:, :, i * F:(i + 1) * F].contiguous() for i in range(wl.n_calls)]
-    out = torch.empty(dec.output_shape(1, F), dtype=torch.float32, device="cuda")
-    pos = [0]
+    outs = [torch.empty(dec.output_shape(1, F), dtype=fdb.pixel_torch_dtype(fmt), device="cuda")
+            for _ in range(NS)]
+    out = outs[0]
+    # stream i starts i * n_calls / NS chunks into the sequence, so the
+    # concurrent streams sit at different positions
+    pos = [i * wl.n_calls // NS for i in range(NS)]
 
     def step():
-        j = pos[0] % wl.n_calls
-        if j == 0:
-            cache.reset()
-        cache.decode_chunk(chunks[j], out)
-        pos[0] += 1
-        return j
+        js = []
+        for i in range(NS):
+            j = pos[i] % wl.n_calls
+            if j == 0:
+                caches[i].reset()
+            js.append(j)
+            pos[i] += 1
+        if NS == 1 and fmt == fdb.FD_PIXELS_F32:
+            cache.decode_chunk(chunks[js[0]], out)
+        elif NS == 1:
+            cache.decode_chunk(chunks[js[0]], out, out_format=fmt)
+        else:
+            fdb.decode_chunks(caches, [chunks[j] for j in js], outs, out_format=fmt)
+        return js
+
+    for i in range(NS):   # bring every stream to its start position
+        for j in range(pos[i]):
+            caches[i].decode_chunk(chunks[j], outs[i], out_format=fmt)
 
     for _ in range(args.warmup):
         step()
@@ -170,21 +196,24 @@ def main() -> int:
     t0 = time.perf_counter()
     for i in range(K):
         ev[i][0].record()
-        j = step()
+        js = step()
         ev[i][1].record()
-        g, a = call_flops(m, F, j * F)
-        flops += g + a
+        for j in js:
+            g, a = call_flops(m, F, j * F)
+            flops += g + a
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     attn_ms, attn_n, attn_work = fdb.fd_probe_read(cache.handle)
     fdb.fd_probe_enable(cache.handle, -1)
-    assert not torch.isnan(out).any().item(), "NaN in decoded pixels"
+    if fmt != fdb.FD_PIXELS_U8:
+        assert not any(torch.isnan(o.float()).any().item() for o in outs), "NaN in decoded pixels"
 
     wall = t1 - t0
     lat = np.array([a.elapsed_time(b) for a, b in ev])
     # sustained dense MFMA throughput of this GPU (after the timed region)
     peak_meas, peak_ghz = fdb.fd_measure_mfma_peak("f16", 100000)
-    frames = K * F * m.r_t
+    frames = K * F * m.r_t * NS
+    fp8 = getattr(m, "mlp_precision", "f16") == "fp8"
     achieved = attn_work / (attn_ms * 1e-3) / 1e12
     result = {
         "metric": METRIC,
@@ -197,7 +226,7 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f16",
+        "dtype": "f16+fp8" if fp8 else "f16",
         "data": "synthetic",
         "config": {
             "workload": wl.name,
@@ -205,6 +234,9 @@ def main() -> int:
             "latent_per_chunk": f"{m.latent_channels}x{F}x{m.latent_h}x{m.latent_w}",
             "pixels_per_chunk": f"3x{F * m.r_t}x{m.out_h}x{m.out_w}",
             "chunks_per_stream": wl.n_calls,
+            "concurrent_streams": NS,
+            "pixel_format": args.pixels,
+            "mlp_gemms": "E4M3 x E4M3 (per-token / per-channel scales)" if fp8 else "fp16",
             "window": m.window,
             "p50_chunk_ms": round(float(np.percentile(lat, 50)), 4),
             "p99_chunk_ms": round(float(np.percentile(lat, 99)), 4),
@@ -234,7 +266,8 @@ def main() -> int:
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, weights, None)
     print(json.dumps(result), flush=True)
-    cache.close()
+    for c in caches:
+        c.close()
     dec.close()
     return 0
 

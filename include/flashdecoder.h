@@ -153,6 +153,15 @@ void fd_kv_cache_destroy(fd_kv_cache* cache);
 fd_status fd_output_shape(const fd_decoder* dec, int32_t batch, int32_t n_frames,
                           int64_t shape[5]);
 
+/* Pixel formats of fd_decode_chunk_as / fd_decode_chunks. Each pixel is first
+ * clamped to [-1, 1] when clamp_output is set, then stored as
+ *   FD_PIXELS_F32   fp32;
+ *   FD_PIXELS_BF16  bf16, rounded to nearest even;
+ *   FD_PIXELS_U8    uint8 = rint(fp32(x * 127.5 + 127.5)), one fp32 rounding of
+ *                   the fused multiply-add, ties to even, limited to 0..255
+ *                   (so -1 -> 0, 0 -> 128, 1 -> 255; 4x fewer bytes than fp32). */
+enum { FD_PIXELS_F32 = 0, FD_PIXELS_BF16 = 1, FD_PIXELS_U8 = 2 };
+
 /* Decode one chunk (Algorithm 1 for n_frames consecutive latent frames).
  *   latent  device pointer, [batch, C', n_frames, H', W'] contiguous, latent_dtype
  *   n_frames 1..max_frames_per_call, a multiple of unit_frames
@@ -165,6 +174,30 @@ fd_status fd_output_shape(const fd_decoder* dec, int32_t batch, int32_t n_frames
  * The cache must not be used by two calls at once. */
 fd_status fd_decode_chunk(const fd_decoder* dec, const void* latent, int32_t latent_dtype,
                           int32_t n_frames, fd_kv_cache* cache, float* out, void* stream);
+
+/* fd_decode_chunk with the pixels in out_format (FD_PIXELS_*): out holds
+ * fd_output_shape elements of 4, 2 or 1 bytes. The decode before the pixel
+ * store is the same, so an FD_PIXELS_U8 or FD_PIXELS_BF16 call equals the rule
+ * above applied to the fp32 pixels of the same call. Unknown formats give
+ * INVALID_ARGUMENT. */
+fd_status fd_decode_chunk_as(const fd_decoder* dec, const void* latent, int32_t latent_dtype,
+                             int32_t n_frames, fd_kv_cache* cache, void* out, int32_t out_format,
+                             void* stream);
+
+/* Multi-stream serving: one chunk of n_frames frames for each of n independent
+ * streams of one decoder, each with its own cache (and so its own position,
+ * ring and workspace): caches[i] decodes latents[i] into outs[i] (layouts and
+ * rules of fd_decode_chunk_as). The decodes run concurrently, each on a HIP
+ * stream owned by its cache (created at the cache's first such call, default
+ * priority), after the work already enqueued on `stream`; `stream` waits for
+ * all of them, so the call is asynchronous on `stream` like fd_decode_chunk.
+ * Each cache's result equals fd_decode_chunk_as on that cache alone. All
+ * arguments are checked before any work is enqueued: n >= 1, no NULL, no
+ * cache twice, every cache from dec, else INVALID_ARGUMENT / STATE. A cache
+ * must not be in use by another call meanwhile. */
+fd_status fd_decode_chunks(const fd_decoder* dec, int32_t n, const void* const* latents,
+                           int32_t latent_dtype, int32_t n_frames, fd_kv_cache* const* caches,
+                           void* const* outs, int32_t out_format, void* stream);
 
 /* fd_decode_chunk that also copies the fp32 residual stream into `trace`
  * (device pointer, fp32) after the embedding and after every block: first the

@@ -60,6 +60,10 @@ struct EpiParams {
   int frames_in = 0;        // latent frames in the call
   int frames_out = 0;       // output frames in the call (frames_in * r_t)
   int clamp = 1;
+  // pixel stores (EPI_PIXEL, EPI_LINEAR_PIXEL) write out_f's memory as fp32
+  // (0), bf16 (1, nearest even) or uint8 (2, rint(fp32(x 127.5 + 127.5))
+  // limited to 0..255)
+  int out_fmt = 0;
   // FP8 GEMM: the accumulator of (row m, column n) is multiplied by
   // row_scale[m] * col_scale[n] before the bias and the epilogue
   const float* row_scale = nullptr;

@@ -283,6 +283,9 @@ struct fd_kv_cache {
   float *sa = nullptr, *sh = nullptr;     // their per-row scales
   float2* rope_t = nullptr;  // temporal RoPE (cos, sin) of the current call
   Probe probe;
+  // fd_decode_chunks: this cache's own stream and its fork / join events
+  hipStream_t own = nullptr;
+  hipEvent_t fork = nullptr, done = nullptr;
 };
 
 namespace {
@@ -534,18 +537,30 @@ fd_status run_stack(Ctx& x, const std::vector<LayerW>& layers, float* xs, int ro
   return FD_OK;
 }
 
-fd_status decode(const fd_decoder* dec, const void* latent, int32_t latent_dtype, int32_t F,
-                 fd_kv_cache* kc, float* out, void* stream, float* trace, size_t trace_elems) {
+// Argument checks of one decode call (no device work).
+fd_status check_decode(const fd_decoder* dec, const void* latent, int32_t latent_dtype, int32_t F,
+                       const fd_kv_cache* kc, const void* out, int32_t out_fmt) {
   if (!dec || !kc || !latent || !out) return fail(FD_ERR_INVALID_ARGUMENT, "NULL argument");
   if (kc->dec != dec) return fail(FD_ERR_STATE, "cache was created by a different decoder");
   const fd_config& c = dec->cfg;
-  const Derived& d = dec->d;
   if (latent_dtype < 0 || latent_dtype > 2)
     return fail(FD_ERR_INVALID_ARGUMENT, "unknown latent dtype %d", latent_dtype);
+  if (out_fmt < FD_PIXELS_F32 || out_fmt > FD_PIXELS_U8)
+    return fail(FD_ERR_INVALID_ARGUMENT, "unknown pixel format %d", out_fmt);
   if (F <= 0 || F > c.max_frames_per_call || F % c.unit_frames)
     return fail(FD_ERR_INVALID_ARGUMENT,
                 "n_frames %d must be in 1..%d and a multiple of unit_frames %d", F,
                 c.max_frames_per_call, c.unit_frames);
+  return FD_OK;
+}
+
+fd_status decode(const fd_decoder* dec, const void* latent, int32_t latent_dtype, int32_t F,
+                 fd_kv_cache* kc, void* out, int32_t out_fmt, void* stream, float* trace,
+                 size_t trace_elems) {
+  fd_status cst = check_decode(dec, latent, latent_dtype, F, kc, out, out_fmt);
+  if (cst != FD_OK) return cst;
+  const fd_config& c = dec->cfg;
+  const Derived& d = dec->d;
   if (trace && trace_elems < fd_trace_elems(dec, kc->batch, F))
     return fail(FD_ERR_INVALID_ARGUMENT, "trace buffer too small");
   hipStream_t s = (hipStream_t)stream;
@@ -594,7 +609,8 @@ fd_status decode(const fd_decoder* dec, const void* latent, int32_t latent_dtype
       const int cs2 = c.out_channels * c.s_out * c.s_out;
       g = gemm_args(kc->h, c.head_hidden, dec->head2_w, MR, cs2, c.head_hidden, fd::EPI_PIXEL,
                     dec->head2_b);
-      g.ep.out_f = out;
+      g.ep.out_f = (float*)out;
+      g.ep.out_fmt = out_fmt;
       g.ep.L = d.L;
       g.ep.r_t = c.r_t;
       g.ep.grid_h = d.grid_h;
@@ -608,7 +624,8 @@ fd_status decode(const fd_decoder* dec, const void* latent, int32_t latent_dtype
     } else {
       const int cs2 = c.out_channels * c.s_out * c.s_out;
       g = gemm_args(kc->a, D, dec->head_w, M, c.r_t * cs2, D, fd::EPI_LINEAR_PIXEL, dec->head_b);
-      g.ep.out_f = out;
+      g.ep.out_f = (float*)out;
+      g.ep.out_fmt = out_fmt;
       g.ep.L = d.L;
       g.ep.r_t = c.r_t;
       g.ep.grid_h = d.grid_h;
@@ -855,6 +872,9 @@ void free_cache(fd_kv_cache* c) {
     (void)hipEventDestroy(r.b);
   }
   for (auto e : c->probe.pool) (void)hipEventDestroy(e);
+  if (c->own) (void)hipStreamDestroy(c->own);
+  if (c->fork) (void)hipEventDestroy(c->fork);
+  if (c->done) (void)hipEventDestroy(c->done);
   delete c;
 }
 
@@ -1051,9 +1071,67 @@ size_t fd_trace_elems(const fd_decoder* dec, int32_t batch, int32_t n_frames) {
 fd_status fd_decode_chunk(const fd_decoder* dec, const void* latent, int32_t latent_dtype,
                           int32_t n_frames, fd_kv_cache* cache, float* out, void* stream) {
   try {
-    return decode(dec, latent, latent_dtype, n_frames, cache, out, stream, nullptr, 0);
+    return decode(dec, latent, latent_dtype, n_frames, cache, out, FD_PIXELS_F32, stream, nullptr, 0);
   } catch (...) {
     return fail(FD_ERR_DEVICE, "unexpected error in fd_decode_chunk");
+  }
+}
+
+fd_status fd_decode_chunk_as(const fd_decoder* dec, const void* latent, int32_t latent_dtype,
+                             int32_t n_frames, fd_kv_cache* cache, void* out, int32_t out_format,
+                             void* stream) {
+  try {
+    return decode(dec, latent, latent_dtype, n_frames, cache, out, out_format, stream, nullptr, 0);
+  } catch (...) {
+    return fail(FD_ERR_DEVICE, "unexpected error in fd_decode_chunk_as");
+  }
+}
+
+fd_status fd_decode_chunks(const fd_decoder* dec, int32_t n, const void* const* latents,
+                           int32_t latent_dtype, int32_t n_frames, fd_kv_cache* const* caches,
+                           void* const* outs, int32_t out_format, void* stream) {
+  if (!dec || n < 1 || !latents || !caches || !outs)
+    return fail(FD_ERR_INVALID_ARGUMENT, "NULL argument or n < 1");
+  for (int i = 0; i < n; ++i) {
+    fd_status st = check_decode(dec, latents[i], latent_dtype, n_frames, caches[i], outs[i], out_format);
+    if (st != FD_OK) return st;
+    for (int j = 0; j < i; ++j)
+      if (caches[j] == caches[i]) return fail(FD_ERR_INVALID_ARGUMENT, "cache %d appears twice", i);
+  }
+  try {
+    int prev_dev = 0;
+    FD_HIP(hipGetDevice(&prev_dev));
+    if (prev_dev != dec->device) FD_HIP(hipSetDevice(dec->device));
+    fd_status st = FD_OK;
+    for (int i = 0; i < n && st == FD_OK; ++i) {  // streams and events, once per cache
+      fd_kv_cache* kc = caches[i];
+      if (!kc->own && hipStreamCreateWithFlags(&kc->own, hipStreamNonBlocking) != hipSuccess)
+        st = fail(FD_ERR_DEVICE, "stream creation failed");
+      else if (!kc->fork && hipEventCreateWithFlags(&kc->fork, hipEventDisableTiming) != hipSuccess)
+        st = fail(FD_ERR_DEVICE, "event creation failed");
+      else if (!kc->done && hipEventCreateWithFlags(&kc->done, hipEventDisableTiming) != hipSuccess)
+        st = fail(FD_ERR_DEVICE, "event creation failed");
+    }
+    hipStream_t s = (hipStream_t)stream;
+    // fork: every cache's stream starts after the work already on `stream`
+    if (st == FD_OK && hipEventRecord(caches[0]->fork, s) != hipSuccess)
+      st = fail(FD_ERR_DEVICE, "event record failed");
+    for (int i = 0; i < n && st == FD_OK; ++i) {
+      fd_kv_cache* kc = caches[i];
+      if (hipStreamWaitEvent(kc->own, caches[0]->fork, 0) != hipSuccess) {
+        st = fail(FD_ERR_DEVICE, "stream wait failed");
+        break;
+      }
+      st = decode(dec, latents[i], latent_dtype, n_frames, kc, outs[i], out_format, kc->own, nullptr, 0);
+      // join: `stream` continues after every cache's decode (also after a
+      // failed one, so no work is left unordered)
+      if (hipEventRecord(kc->done, kc->own) != hipSuccess || hipStreamWaitEvent(s, kc->done, 0) != hipSuccess)
+        if (st == FD_OK) st = fail(FD_ERR_DEVICE, "join failed");
+    }
+    if (prev_dev != dec->device) (void)hipSetDevice(prev_dev);
+    return st;
+  } catch (...) {
+    return fail(FD_ERR_DEVICE, "unexpected error in fd_decode_chunks");
   }
 }
 
@@ -1062,7 +1140,8 @@ fd_status fd_decode_chunk_trace(const fd_decoder* dec, const void* latent, int32
                                 float* trace, size_t trace_elems) {
   if (!trace) return fail(FD_ERR_INVALID_ARGUMENT, "trace is NULL");
   try {
-    return decode(dec, latent, latent_dtype, n_frames, cache, out, stream, trace, trace_elems);
+    return decode(dec, latent, latent_dtype, n_frames, cache, out, FD_PIXELS_F32, stream, trace,
+                  trace_elems);
   } catch (...) {
     return fail(FD_ERR_DEVICE, "unexpected error in fd_decode_chunk_trace");
   }

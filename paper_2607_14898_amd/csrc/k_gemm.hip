@@ -88,6 +88,41 @@ __device__ __forceinline__ int64_t col_off(const EpiParams& p, int col) {
   }
 }
 
+// One output pixel: clamped to [-1, 1] if requested, then in the destination
+// format (fp32; bf16 rounded to nearest even; uint8 = rint of the fp32 fma
+// x 127.5 + 127.5, ties to even, limited to 0..255).
+__device__ __forceinline__ float px_clamp(const EpiParams& p, float v) {
+  return p.clamp ? fminf(1.f, fmaxf(-1.f, v)) : v;
+}
+__device__ __forceinline__ uint32_t px_u8(float v) {
+  return (uint32_t)fminf(255.f, fmaxf(0.f, rintf(fmaf(v, 127.5f, 127.5f))));
+}
+__device__ __forceinline__ void px_store(const EpiParams& p, int64_t off, float v) {
+  v = px_clamp(p, v);
+  if (p.out_fmt == 0) p.out_f[off] = v;
+  else if (p.out_fmt == 1) reinterpret_cast<__hip_bfloat16*>(p.out_f)[off] = __float2bfloat16(v);
+  else reinterpret_cast<uint8_t*>(p.out_f)[off] = (uint8_t)px_u8(v);
+}
+// Four consecutive pixels at an offset that is a multiple of 4 (16-, 8- or
+// 4-byte store).
+__device__ __forceinline__ void px_store4(const EpiParams& p, int64_t off, const float (&v)[4]) {
+  float c[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) c[e] = px_clamp(p, v[e]);
+  if (p.out_fmt == 0) {
+    *reinterpret_cast<float4*>(p.out_f + off) = make_float4(c[0], c[1], c[2], c[3]);
+  } else if (p.out_fmt == 1) {
+    __hip_bfloat16 o4[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o4[e] = __float2bfloat16(c[e]);
+    *reinterpret_cast<uint2*>(reinterpret_cast<__hip_bfloat16*>(p.out_f) + off) =
+        *reinterpret_cast<const uint2*>(o4);
+  } else {
+    *reinterpret_cast<uint32_t*>(reinterpret_cast<uint8_t*>(p.out_f) + off) =
+        px_u8(c[0]) | (px_u8(c[1]) << 8) | (px_u8(c[2]) << 16) | (px_u8(c[3]) << 24);
+  }
+}
+
 // Store one value (bias already added) at the precomputed offset.
 template <int EPI, typename TA>
 __device__ __forceinline__ void epi_store(const EpiParams& p, int64_t off, float c) {
@@ -102,7 +137,7 @@ __device__ __forceinline__ void epi_store(const EpiParams& p, int64_t off, float
   } else if constexpr (EPI == EPI_STORE_GELU) {
     ((TA*)p.out_a)[off] = to_act<TA>(gelu_f(c));
   } else if constexpr (EPI == EPI_PIXEL || EPI == EPI_LINEAR_PIXEL) {
-    p.out_f[off] = p.clamp ? fminf(1.f, fmaxf(-1.f, c)) : c;
+    px_store(p, off, c);
   }
 }
 
@@ -490,10 +525,7 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
             if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_TUP) {
               *reinterpret_cast<f4*>(ep.out_f + off) = f4{v[0], v[1], v[2], v[3]};
             } else if constexpr (EPI == EPI_PIXEL || EPI == EPI_LINEAR_PIXEL) {
-              if (ep.clamp)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) v[e] = fminf(1.f, fmaxf(-1.f, v[e]));
-              *reinterpret_cast<f4*>(ep.out_f + off) = f4{v[0], v[1], v[2], v[3]};
+              px_store4(ep, off, v);
             } else {
               T o4[4];
 #pragma unroll

@@ -80,6 +80,9 @@ def load_library() -> ctypes.CDLL:
         "fd_output_shape": (I32, [P, I32, I32, ctypes.POINTER(I64)]),
         "fd_decode_chunk": (I32, [P, P, I32, I32, P, P, P]),
         "fd_decode_chunk_trace": (I32, [P, P, I32, I32, P, P, P, P, SZ]),
+        "fd_decode_chunk_as": (I32, [P, P, I32, I32, P, P, I32, P]),
+        "fd_decode_chunks": (I32, [P, I32, ctypes.POINTER(P), I32, I32, ctypes.POINTER(P),
+                                   ctypes.POINTER(P), I32, P]),
         "fd_trace_elems": (SZ, [P, I32, I32]),
         "fd_probe_enable": (I32, [P, I32]),
         "fd_probe_read": (I32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64),
@@ -216,6 +219,45 @@ def fd_decode_chunk(dec: int, latent, n_frames: int, cache: int, out, stream=Non
                                           cache, out.data_ptr(), _stream_handle(stream)))
 
 
+FD_PIXELS_F32, FD_PIXELS_BF16, FD_PIXELS_U8 = 0, 1, 2
+
+
+def pixel_torch_dtype(out_format: int):
+    import torch
+    return {FD_PIXELS_F32: torch.float32, FD_PIXELS_BF16: torch.bfloat16,
+            FD_PIXELS_U8: torch.uint8}[out_format]
+
+
+def _check_out(out, out_format: int) -> None:
+    if out.dtype != pixel_torch_dtype(out_format) or not out.is_contiguous():
+        raise ValueError(f"out must be a contiguous {pixel_torch_dtype(out_format)} tensor")
+
+
+def fd_decode_chunk_as(dec: int, latent, n_frames: int, cache: int, out, out_format: int,
+                       stream=None) -> None:
+    """fd_decode_chunk with pixels in out_format (FD_PIXELS_*); out's dtype must match."""
+    _check_out(out, out_format)
+    _check(load_library().fd_decode_chunk_as(dec, latent.data_ptr(), _latent_dtype(latent), n_frames,
+                                             cache, out.data_ptr(), out_format, _stream_handle(stream)))
+
+
+def fd_decode_chunks(dec: int, latents, n_frames: int, caches, outs, out_format: int,
+                     stream=None) -> None:
+    """One chunk for each of len(caches) independent caches, run concurrently."""
+    n = len(caches)
+    if not (len(latents) == len(outs) == n):
+        raise ValueError("latents, caches and outs must have the same length")
+    dts = {_latent_dtype(z) for z in latents}
+    if len(dts) != 1:
+        raise ValueError("all latents must have the same dtype")
+    for o in outs:
+        _check_out(o, out_format)
+    arr = ctypes.c_void_p * n
+    _check(load_library().fd_decode_chunks(
+        dec, n, arr(*[z.data_ptr() for z in latents]), dts.pop(), n_frames, arr(*caches),
+        arr(*[o.data_ptr() for o in outs]), out_format, _stream_handle(stream)))
+
+
 def fd_decode_chunk_trace(dec: int, latent, n_frames: int, cache: int, out, trace,
                           stream=None) -> None:
     _check(load_library().fd_decode_chunk_trace(
@@ -327,14 +369,19 @@ class KvCache:
     def position(self) -> int:
         return fd_kv_cache_position(self.handle)
 
-    def decode_chunk(self, latent, out=None, stream=None):
-        """Decode latent [B, C', F, H', W'] (torch, on GPU); returns fp32 pixels."""
+    def decode_chunk(self, latent, out=None, stream=None, out_format: int = FD_PIXELS_F32):
+        """Decode latent [B, C', F, H', W'] (torch, on GPU); returns the pixels
+        (fp32, or bf16 / uint8 for the other FD_PIXELS_* formats)."""
         import torch
         F = latent.shape[2]
         if out is None:
-            out = torch.empty(self.decoder.output_shape(self.batch, F), dtype=torch.float32,
-                              device=latent.device)
-        fd_decode_chunk(self.decoder.handle, latent.contiguous(), F, self.handle, out, stream)
+            out = torch.empty(self.decoder.output_shape(self.batch, F),
+                              dtype=pixel_torch_dtype(out_format), device=latent.device)
+        if out_format == FD_PIXELS_F32:
+            fd_decode_chunk(self.decoder.handle, latent.contiguous(), F, self.handle, out, stream)
+        else:
+            fd_decode_chunk_as(self.decoder.handle, latent.contiguous(), F, self.handle, out,
+                               out_format, stream)
         return out
 
     def close(self) -> None:
@@ -347,3 +394,19 @@ class KvCache:
             self.close()
         except Exception:
             pass
+
+
+def decode_chunks(caches, latents, outs=None, out_format: int = FD_PIXELS_F32, stream=None):
+    """Concurrent decode of one chunk per KvCache (all of one Decoder, distinct);
+    returns the list of pixel tensors."""
+    import torch
+    dec = caches[0].decoder
+    if any(c.decoder is not dec for c in caches):
+        raise ValueError("all caches must belong to one Decoder")
+    F = latents[0].shape[2]
+    latents = [z.contiguous() for z in latents]
+    if outs is None:
+        outs = [torch.empty(dec.output_shape(c.batch, F), dtype=pixel_torch_dtype(out_format),
+                            device=z.device) for c, z in zip(caches, latents)]
+    fd_decode_chunks(dec.handle, latents, F, [c.handle for c in caches], outs, out_format, stream)
+    return outs

@@ -196,3 +196,14 @@ def test_e4m3_gemm_rejects_bad_arguments_before_any_device_call(m, n, k, lda, ep
     st = lib.fd_gemm_e4m3_device(None, lda, None, None, None, None, m, n, k, epi, None, ld_out, None)
     assert st == fdb.FD_ERR_INVALID_ARGUMENT
     assert lib.fd_last_error().decode() != ""
+
+
+def test_serving_entry_points_reject_bad_arguments_before_any_device_call():
+    lib = _lib()
+    P = ctypes.c_void_p
+    arr = (P * 1)(None)
+    assert lib.fd_decode_chunk_as(None, None, 0, 1, None, None, fdb.FD_PIXELS_U8, None) == \
+        fdb.FD_ERR_INVALID_ARGUMENT
+    assert lib.fd_decode_chunks(None, 1, arr, 0, 1, arr, arr, 0, None) == fdb.FD_ERR_INVALID_ARGUMENT
+    assert lib.fd_decode_chunks(None, 0, None, 0, 1, None, None, 0, None) == fdb.FD_ERR_INVALID_ARGUMENT
+    assert fdb.FD_PIXELS_F32 == 0 and fdb.FD_PIXELS_BF16 == 1 and fdb.FD_PIXELS_U8 == 2

@@ -5,6 +5,7 @@ Usage: python -m paper_2607_14898_amd.build  (or __graft_entry__.build()).
 from __future__ import annotations
 
 import os
+import re
 import subprocess
 import sys
 from concurrent.futures import ThreadPoolExecutor
@@ -20,13 +21,36 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          "-I" + os.path.join(ROOT, "include")]
 
 
+def _scratch_users(remarks: str) -> list:
+    """Kernels whose resource remarks report scratch memory or vector-register
+    spills (scalar-register spills go to vector-register lanes, not memory)."""
+    bad, name = [], None
+    for line in remarks.splitlines():
+        m = re.search(r"remark: Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            continue
+        m = re.search(r"remark:\s+(ScratchSize \[bytes/lane\]|VGPRs Spill): (\d+)", line)
+        if m and name and int(m.group(2)) > 0:
+            bad.append(f"{name}: {m.group(1)} = {m.group(2)}")
+    return bad
+
+
 def _compile(src: str, obj: str) -> None:
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(PKG, src), "-o", obj]
+    # every GPU kernel must run from registers and LDS: the compiler's
+    # resource remarks are checked for scratch use and spills
+    hip = src.endswith(".hip")
+    cmd = [HIPCC, *FLAGS, *(["-Rpass-analysis=kernel-resource-usage"] if hip else []),
+           "-c", os.path.join(PKG, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")
+    bad = _scratch_users(r.stderr) if hip else []
+    if bad:
+        raise RuntimeError(f"{src}: kernels using scratch memory:\n" + "\n".join(bad))
     err = "\n".join(l for l in r.stderr.splitlines() if "packed-fp32-ops" not in l
-                    and "not a recognized feature" not in l)
+                    and "not a recognized feature" not in l and "remark:" not in l
+                    and not re.match(r"^\s*(\d+ \||\|)", l))
     if "warning" in err:
         sys.stderr.write(err + "\n")
 

@@ -11,7 +11,8 @@
 // wave owns 64 queries as two 32-query MFMA blocks and computes S^T = K Q^T
 // with the 32x32x16 MFMA, so a lane holds one query and 16 key scores per 32-key
 // block: the softmax max needs one cross-half exchange per tile and the row
-// sums stay lane-local (fp32 adds of the probabilities) until the end. K
+// sums stay lane-local until the end (per tile a packed-f16 sum of the f16
+// probabilities for fp16 operands, an fp32 sum for bf16). K
 // rows are fed to the MFMA in the order that makes the score registers of a
 // lane exactly the B operand of the following O^T += V^T P^T MFMA, so P never
 // leaves registers. Queries are pre-scaled by log2(e) / sqrt(D_h), and each
@@ -23,6 +24,7 @@
 #include "fd_kernels.h"
 
 #include <hip/hip_bf16.h>
+#include <type_traits>
 
 namespace fd {
 namespace {
@@ -249,8 +251,6 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
     auto exp_tile = [&]() {
 #pragma unroll
       for (int qb = 0; qb < NQB; ++qb) {
-        // row sum of the fp32 probabilities by a pairwise tree (plain adds
-        // overlap the MFMAs; the packed-f16 dot instruction does not)
         float t[32];
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
@@ -263,11 +263,30 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
               t[(kb * 2 + h) * 8 + e] = p;
             }
           }
+        if constexpr (std::is_same<T, _Float16>::value) {
+          // row sum of the f16 probabilities the P V MFMA multiplies, by a
+          // packed-f16 pairwise tree (16 instructions instead of 31 fp32
+          // adds); an overflow to inf raises the shift like any large sum
+          typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+          h2 u[16];
 #pragma unroll
-        for (int w = 16; w >= 1; w >>= 1)
+          for (int st = 0; st < 4; ++st)
 #pragma unroll
-          for (int i = 0; i < w; ++i) t[i] = t[i] + t[i + w];
-        ls[qb] = t[0];
+            for (int e = 0; e < 4; ++e) u[st * 4 + e] = h2{pf[qb][st][2 * e], pf[qb][st][2 * e + 1]};
+#pragma unroll
+          for (int w = 8; w >= 1; w >>= 1)
+#pragma unroll
+            for (int i = 0; i < w; ++i) u[i] = u[i] + u[i + w];
+          ls[qb] = (float)u[0][0] + (float)u[0][1];
+        } else {
+          // row sum of the fp32 probabilities by a pairwise tree (plain adds
+          // overlap the MFMAs; the packed-f16 dot instruction does not)
+#pragma unroll
+          for (int w = 16; w >= 1; w >>= 1)
+#pragma unroll
+            for (int i = 0; i < w; ++i) t[i] = t[i] + t[i + w];
+          ls[qb] = t[0];
+        }
       }
     };
     scores();
@@ -350,6 +369,7 @@ template <int DH>
 __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a, int q_tiles) {
   __shared__ float sk[64][DH + 1];
   __shared__ float sv[DH][65];
+  __shared__ float ss[64][65];  // scores of a key tile, one column per thread (query)
   const int tid = threadIdx.x;
   const int n = blockIdx.y;
   const int bx = blockIdx.x;
@@ -381,19 +401,19 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a, int q_tiles) {
       }
       __syncthreads();
       const int nk = min(64, a.U - k0);
-      float sc[64];
       float mx = m_run;
       for (int j = 0; j < nk; ++j) {
         float acc = 0.f;
         for (int d = 0; d < DH; ++d) acc = fmaf(q[d], sk[j][d], acc);
-        sc[j] = acc * a.scale;
-        mx = fmaxf(mx, sc[j]);
+        const float sc = acc * a.scale;
+        ss[j][tid] = sc;
+        mx = fmaxf(mx, sc);
       }
       const float alpha = expf(m_run - mx);
       for (int d = 0; d < DH; ++d) o[d] *= alpha;
       l_run *= alpha;
       for (int j = 0; j < nk; ++j) {
-        const float p = expf(sc[j] - mx);
+        const float p = expf(ss[j][tid] - mx);
         l_run += p;
         for (int d = 0; d < DH; ++d) o[d] = fmaf(p, sv[d][j], o[d]);
       }

@@ -97,26 +97,29 @@ __device__ __forceinline__ float px_clamp(const EpiParams& p, float v) {
 __device__ __forceinline__ uint32_t px_u8(float v) {
   return (uint32_t)fminf(255.f, fmaxf(0.f, rintf(fmaf(v, 127.5f, 127.5f))));
 }
+// PXF: the format when known at compile time, -1 to read p.out_fmt
+template <int PXF>
 __device__ __forceinline__ void px_store(const EpiParams& p, int64_t off, float v) {
+  const int f = PXF >= 0 ? PXF : p.out_fmt;
   v = px_clamp(p, v);
-  if (p.out_fmt == 0) p.out_f[off] = v;
-  else if (p.out_fmt == 1) reinterpret_cast<__hip_bfloat16*>(p.out_f)[off] = __float2bfloat16(v);
+  if (f == 0) p.out_f[off] = v;
+  else if (f == 1) reinterpret_cast<__hip_bfloat16*>(p.out_f)[off] = __float2bfloat16(v);
   else reinterpret_cast<uint8_t*>(p.out_f)[off] = (uint8_t)px_u8(v);
 }
 // Four consecutive pixels at an offset that is a multiple of 4 (16-, 8- or
 // 4-byte store).
+template <int PXF>
 __device__ __forceinline__ void px_store4(const EpiParams& p, int64_t off, const float (&v)[4]) {
+  static_assert(PXF >= 0, "vector pixel stores take a compile-time format");
   float c[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) c[e] = px_clamp(p, v[e]);
-  if (p.out_fmt == 0) {
+  if constexpr (PXF == 0) {
     *reinterpret_cast<float4*>(p.out_f + off) = make_float4(c[0], c[1], c[2], c[3]);
-  } else if (p.out_fmt == 1) {
-    __hip_bfloat16 o4[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) o4[e] = __float2bfloat16(c[e]);
-    *reinterpret_cast<uint2*>(reinterpret_cast<__hip_bfloat16*>(p.out_f) + off) =
-        *reinterpret_cast<const uint2*>(o4);
+  } else if constexpr (PXF == 1) {  // packed from the bit patterns (no stack array)
+    auto bits = [](float x) { return (uint32_t)__bfloat16_as_ushort(__float2bfloat16(x)); };
+    *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(p.out_f) + off) =
+        make_uint2(bits(c[0]) | (bits(c[1]) << 16), bits(c[2]) | (bits(c[3]) << 16));
   } else {
     *reinterpret_cast<uint32_t*>(reinterpret_cast<uint8_t*>(p.out_f) + off) =
         px_u8(c[0]) | (px_u8(c[1]) << 8) | (px_u8(c[2]) << 16) | (px_u8(c[3]) << 24);
@@ -124,7 +127,7 @@ __device__ __forceinline__ void px_store4(const EpiParams& p, int64_t off, const
 }
 
 // Store one value (bias already added) at the precomputed offset.
-template <int EPI, typename TA>
+template <int EPI, typename TA, int PXF = -1>
 __device__ __forceinline__ void epi_store(const EpiParams& p, int64_t off, float c) {
   if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_TUP) {
     p.out_f[off] = c;
@@ -137,7 +140,7 @@ __device__ __forceinline__ void epi_store(const EpiParams& p, int64_t off, float
   } else if constexpr (EPI == EPI_STORE_GELU) {
     ((TA*)p.out_a)[off] = to_act<TA>(gelu_f(c));
   } else if constexpr (EPI == EPI_PIXEL || EPI == EPI_LINEAR_PIXEL) {
-    px_store(p, off, c);
+    px_store<PXF>(p, off, c);
   }
 }
 
@@ -203,7 +206,7 @@ __device__ __forceinline__ int div_small(int x, int d, float inv) {
   return q + (r >= d) - (r < 0);
 }
 
-template <int EPI, typename T, int FM, int FN, bool FAST_RMW>
+template <int EPI, typename T, int FM, int FN, bool FAST_RMW, int PXF = 0>
 __device__ __forceinline__ void store_tile(const EpiParams& ep, const f32x16 (&acc)[FM][FN], int r0,
                                            int c0, int M, int N, int lr, int lk, float* ws) {
   if constexpr (EPI == EPI_QKV) {
@@ -383,7 +386,7 @@ __device__ __forceinline__ void store_tile(const EpiParams& ep, const f32x16 (&a
 #pragma unroll
           for (int r = 0; r < 16; ++r)
 #pragma unroll
-            for (int j = 0; j < FN; ++j) epi_store<EPI, T>(ep, ro[r] + coff[j], acc[i][j][r] + cb[j]);
+            for (int j = 0; j < FN; ++j) epi_store<EPI, T, PXF>(ep, ro[r] + coff[j], acc[i][j][r] + cb[j]);
         }
         continue;
       }
@@ -403,7 +406,7 @@ __device__ __forceinline__ void store_tile(const EpiParams& ep, const f32x16 (&a
         for (int r = 0; r < 16; ++r)
 #pragma unroll
           for (int j = 0; j < FN; ++j)
-            if (rok[r] && cok[j]) epi_store<EPI, T>(ep, ro[r] + coff[j], acc[i][j][r] + cb[j]);
+            if (rok[r] && cok[j]) epi_store<EPI, T, PXF>(ep, ro[r] + coff[j], acc[i][j][r] + cb[j]);
       }
     }
   }
@@ -415,7 +418,7 @@ __device__ __forceinline__ void store_tile(const EpiParams& ep, const f32x16 (&a
 // 4 lk + 0..3. Every destination access covers those four columns at once (one
 // 16-byte fp32 or 8-byte 16-bit access) whenever the four land contiguously;
 // vec == false (a ragged or unaligned destination) stores element by element.
-template <int EPI, typename T, int FM, int FN, bool SCALED = false>
+template <int EPI, typename T, int FM, int FN, bool SCALED = false, int PXF = 0>
 __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (&acc)[FM][FN], int r0,
                                              int c0, int M, int N, int lr, int lk, bool vec) {
   // SCALED (FP8 GEMM, SwiGLU only): each accumulator is multiplied by its
@@ -489,7 +492,7 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
             for (int e = 0; e < 4; ++e) {
               const int n = c0 + j * 32 + 8 * q + 4 * lk + e;
               if (rok[i] && n < N)
-                epi_store<EPI, T>(ep, ro[i] + col_off<EPI>(ep, n), acc[i][j][4 * q + e] + cb[q][e]);
+                epi_store<EPI, T, PXF>(ep, ro[i] + col_off<EPI>(ep, n), acc[i][j][4 * q + e] + cb[q][e]);
             }
         continue;
       }
@@ -525,7 +528,7 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
             if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_TUP) {
               *reinterpret_cast<f4*>(ep.out_f + off) = f4{v[0], v[1], v[2], v[3]};
             } else if constexpr (EPI == EPI_PIXEL || EPI == EPI_LINEAR_PIXEL) {
-              px_store4(ep, off, v);
+              px_store4<PXF>(ep, off, v);
             } else {
               T o4[4];
 #pragma unroll
@@ -720,9 +723,19 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
   static_assert(EPI != EPI_QKV || NW * 32 * 68 * 4 <= NS * STAGE * 16, "QKV epilogue staging fits the stage buffers");
   if constexpr (kTransposed<EPI>)
     store_tile_t<EPI, T, FM, FN>(ep, acc, m0 + wm0, n0 + wn0, M, N, lr, lk, vec_store != 0);
-  else
+  else if constexpr (EPI == EPI_PIXEL || EPI == EPI_LINEAR_PIXEL) {
+    // one instantiation per pixel format, chosen once per tile (a format test
+    // per store makes the epilogue loops too large to unroll, and the
+    // accumulators would go to scratch memory)
+    constexpr bool R = !(C::NW == 4 && C::MIN_BLOCKS == 1);
+    float* ws = reinterpret_cast<float*>(lds);
+    if (ep.out_fmt == 0) store_tile<EPI, T, FM, FN, R, 0>(ep, acc, m0 + wm0, n0 + wn0, M, N, lr, lk, ws);
+    else if (ep.out_fmt == 1) store_tile<EPI, T, FM, FN, R, 1>(ep, acc, m0 + wm0, n0 + wn0, M, N, lr, lk, ws);
+    else store_tile<EPI, T, FM, FN, R, 2>(ep, acc, m0 + wm0, n0 + wn0, M, N, lr, lk, ws);
+  } else {
     store_tile<EPI, T, FM, FN, !(C::NW == 4 && C::MIN_BLOCKS == 1)>(ep, acc, m0 + wm0, n0 + wn0, M, N, lr, lk,
                                                                    reinterpret_cast<float*>(lds));
+  }
 }
 
 // ---------------------------------------------------------------------------

@@ -39,3 +39,22 @@ def test_workload_shapes():
     assert wl.n_calls == 32 and wl.frames_per_call == 1
     m4 = MODELS["xl-480p"]
     assert (m4.tokens_per_frame, m4.out_h, m4.out_w) == (1560, 480, 832)
+
+
+def test_build_rejects_kernels_that_use_scratch_memory():
+    """build() reads the compiler's resource remarks: scratch memory and
+    vector-register spills fail it, scalar spills (to vector lanes) do not."""
+    from paper_2607_14898_amd.build import _scratch_users
+    remarks = """
+x.hip:1:1: remark: Function Name: kA [-Rpass-analysis=kernel-resource-usage]
+x.hip:1:1: remark:     ScratchSize [bytes/lane]: 0 [-Rpass-analysis=kernel-resource-usage]
+x.hip:1:1: remark:     SGPRs Spill: 31 [-Rpass-analysis=kernel-resource-usage]
+x.hip:1:1: remark:     VGPRs Spill: 0 [-Rpass-analysis=kernel-resource-usage]
+x.hip:9:1: remark: Function Name: kB [-Rpass-analysis=kernel-resource-usage]
+x.hip:9:1: remark:     ScratchSize [bytes/lane]: 272 [-Rpass-analysis=kernel-resource-usage]
+x.hip:9:1: remark:     VGPRs Spill: 0 [-Rpass-analysis=kernel-resource-usage]
+x.hip:20:1: remark: Function Name: kC [-Rpass-analysis=kernel-resource-usage]
+x.hip:20:1: remark:     ScratchSize [bytes/lane]: 0 [-Rpass-analysis=kernel-resource-usage]
+x.hip:20:1: remark:     VGPRs Spill: 12 [-Rpass-analysis=kernel-resource-usage]
+"""
+    assert _scratch_users(remarks) == ["kB: ScratchSize [bytes/lane] = 272", "kC: VGPRs Spill = 12"]

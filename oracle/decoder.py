@@ -44,6 +44,7 @@ __all__ = [
     "decode_stream", "block_forward", "token_positions", "block_forward_rows",
     "stack_final", "temporal_up_rows", "head_rows", "e4m3_round", "quant_rows_e4m3",
     "quant_weight_rows_e4m3", "e4m3_decode", "gemm_e4m3", "pixels_to_u8", "pixels_to_bf16_bits",
+    "quant_static_e4m3", "calibrate_fp8_static",
 ]
 
 # --------------------------------------------------------------------------
@@ -120,6 +121,17 @@ def quant_weight_rows_e4m3(w: np.ndarray):
     """Per-output-channel quantisation of a weight [N, K]: the same rule as
     quant_rows_e4m3 applied to each row of W (the static weight scales)."""
     return quant_rows_e4m3(w)
+
+
+def quant_static_e4m3(a: np.ndarray, amax: float):
+    """Static (calibrated) per-tensor quantisation of activations [M, K] with
+    a fixed amplitude amax: inv = fp32(448 / amax), codes e4m3(fp32(a * inv))
+    -- values beyond amax saturate at +-448 -- and scale s = fp32(amax / 448).
+    Returns (codes as float64 [M, K], s as float64)."""
+    am = np.float32(amax)
+    inv = np.float32(448.0) / am
+    codes = e4m3_round((np.asarray(a, dtype=np.float32) * inv).astype(np.float32))
+    return codes, float(am / np.float32(448.0))
 
 
 def e4m3_decode(codes: np.ndarray) -> np.ndarray:
@@ -326,6 +338,36 @@ def _fp8_linear(x: np.ndarray, w: np.ndarray, b: np.ndarray) -> np.ndarray:
     return (qx @ qw.T) * sx[:, None] * sw[None, :] + b
 
 
+# Calibration recorder: when a dict, the per-token FP8 MLP raises
+# _FP8_RECORD[p] = [amax of the MLP input, amax of the fp16 SwiGLU output]
+# (fp32 values) for every block prefix p it runs.
+_FP8_RECORD: Optional[Dict[str, List[float]]] = None
+
+
+def _fp8_static_linear(x: np.ndarray, amax: float, w: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """x W^T + b with x quantised per tensor at the static amplitude amax and
+    W per output channel: (codes_x codes_W^T) * s_x * s_W[None, :] + b."""
+    qx, sx = quant_static_e4m3(x, amax)
+    qw, sw = quant_weight_rows_e4m3(w)
+    return (qx @ qw.T) * sx * sw[None, :] + b
+
+
+def calibrate_fp8_static(cfg, W, z: np.ndarray, frames_per_call: int = 1) -> Dict[str, List[float]]:
+    """Static activation amplitudes of the FP8 MLP ("static-calibrated", Sec.
+    4.6): decode the calibration latents z with per-token scales and take, for
+    every block, the largest |value| of its MLP input (fp32) and of its fp16
+    SwiGLU output over all rows. Returns {block prefix: [amax_in, amax_hid]}."""
+    from dataclasses import replace as _rp
+    global _FP8_RECORD
+    rec: Dict[str, List[float]] = {}
+    _FP8_RECORD = rec
+    try:
+        decode_stream(_rp(cfg, mlp_precision="fp8"), W, z, frames_per_call)
+    finally:
+        _FP8_RECORD = None
+    return rec
+
+
 def _mlp(cfg, W, p: str, a: np.ndarray) -> np.ndarray:
     """Reading: SwiGLU with hidden width mlp_hidden (rows gate | up of w13);
     the GELU form is the plain two-matrix MLP.
@@ -334,13 +376,26 @@ def _mlp(cfg, W, p: str, a: np.ndarray) -> np.ndarray:
     GEMMs take E4M3 operands: the MLP input per token, the weights per output
     channel, and the SwiGLU output per token after it is stored in fp16 (the
     precision the hidden activation is kept in between the two GEMMs)."""
-    if getattr(cfg, "mlp_precision", "f16") == "fp8":
+    prec = getattr(cfg, "mlp_precision", "f16")
+    if prec == "fp8":
         if cfg.mlp_kind != "swiglu":
             raise ValueError("the FP8 MLP is defined for the SwiGLU form")
         H = cfg.mlp_hidden
         y = _fp8_linear(a, W[p + ".w13"], W[p + ".b13"])
         h = (silu(y[:, :H]) * y[:, H:]).astype(np.float16).astype(np.float64)
+        if _FP8_RECORD is not None:
+            r = _FP8_RECORD.setdefault(p, [0.0, 0.0])
+            r[0] = max(r[0], float(np.abs(np.asarray(a, np.float32)).max()))
+            r[1] = max(r[1], float(np.abs(h).max()))
         return _fp8_linear(h, W[p + ".w2"], W[p + ".b2"])
+    if prec == "fp8s":
+        # static-calibrated: per-tensor amplitudes W[p + ".amax_in"], W[p + ".amax_hid"]
+        if cfg.mlp_kind != "swiglu":
+            raise ValueError("the FP8 MLP is defined for the SwiGLU form")
+        H = cfg.mlp_hidden
+        y = _fp8_static_linear(a, float(W[p + ".amax_in"]), W[p + ".w13"], W[p + ".b13"])
+        h = (silu(y[:, :H]) * y[:, H:]).astype(np.float16).astype(np.float64)
+        return _fp8_static_linear(h, float(W[p + ".amax_hid"]), W[p + ".w2"], W[p + ".b2"])
     if cfg.mlp_kind == "swiglu":
         H = cfg.mlp_hidden
         y = a @ W[p + ".w13"].T + W[p + ".b13"]

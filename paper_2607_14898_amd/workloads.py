@@ -58,7 +58,10 @@ class ModelConfig:
     unit_frames: int = 1        # latent frames per causal unit
     out_channels: int = 3       # C (RGB)
     clamp_output: bool = True
-    mlp_precision: str = "f16"  # "f16" (the compute dtype) | "fp8" (E4M3 MLP GEMMs, Sec. 4.6)
+    # "f16" (the compute dtype) | "fp8" (E4M3 MLP GEMMs, per-token activation
+    # scales) | "fp8s" (E4M3 MLP GEMMs, static per-tensor activation scales;
+    # Sec. 4.6 "static-calibrated FP8")
+    mlp_precision: str = "f16"
 
     @property
     def head_dim(self) -> int:
@@ -195,6 +198,9 @@ class Workload:
     weight_seed: int
     latent_seed: int
     batch: int = 1
+    # static FP8 amplitudes (MLP input, SwiGLU output) of every block, for the
+    # "fp8s" models when a job gives fixed scales instead of calibrating
+    fp8_amax: Tuple[float, float] = (6.0, 10.0)
 
     @property
     def total_frames(self) -> int:
@@ -273,6 +279,11 @@ WORKLOADS = {
                                    weight_seed=0, latent_seed=103),
     "xl-720p-chunk-fp8": Workload("xl-720p-chunk-fp8", replace(XL_720P, mlp_precision="fp8"), 4, 1,
                                   weight_seed=0, latent_seed=104),
+    # static-calibrated FP8 MLP (per-tensor activation scales)
+    "xl-720p-stream-fp8s": Workload("xl-720p-stream-fp8s", replace(XL_720P, mlp_precision="fp8s"), 1, 32,
+                                    weight_seed=0, latent_seed=105),
+    "xl-480p-stream-fp8s": Workload("xl-480p-stream-fp8s", replace(XL_480P, mlp_precision="fp8s"), 1, 16,
+                                    weight_seed=0, latent_seed=103),
     # Wan2.2 latent space (Table 2's second block)
     "xl-wan22-480p-stream": Workload("xl-wan22-480p-stream", XL_WAN22_480P, 1, 16,
                                      weight_seed=4, latent_seed=106),

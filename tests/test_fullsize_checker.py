@@ -98,3 +98,15 @@ def test_teacher_forced_checker_fp8_catches_a_wrong_channel_scale():
     out, traces = _fp8_traces(m, W, z, 2, W_gen=Wbad)
     with pytest.raises(AssertionError, match="bb.1"):
         teacher_forced_check(m, W, z, out, traces, n_rows=20, log=lambda t: None)
+
+
+def test_teacher_forced_checker_static_fp8_on_oracle_traces():
+    """The same branch with static per-tensor FP8 amplitudes."""
+    m = replace(MODELS["xl-720p"], **dict(FP8_SMALL, mlp_precision="fp8s"))
+    W = make_weights(m, 3)
+    for p in [f"bb.{i}" for i in range(m.n_backbone_blocks)] + [f"rf.{i}" for i in range(m.n_refine_blocks)]:
+        W[p + ".amax_in"], W[p + ".amax_hid"] = 4.0, 2.0
+    z = make_latents(m, 2, 4)
+    out, traces = _fp8_traces(m, W, z, 2)
+    worst, pe = teacher_forced_check(m, W, z, out, traces, n_rows=20, log=lambda t: None)
+    assert worst < 1e-10 and pe < 1e-10

@@ -579,3 +579,71 @@ def test_bf16_pixels_match_torch_rounding():
     x = np.concatenate([x, ties.view(np.float32)])
     ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
     assert np.array_equal(pixels_to_bf16_bits(x), ref)
+
+
+# --------------------------------------------------------------------------
+# Static-calibrated FP8 MLP (Sec. 4.6 "-Opt": static-calibrated FP8 for all MLP layers)
+# --------------------------------------------------------------------------
+
+def test_static_e4m3_saturates_beyond_amax_and_reduces_to_the_per_token_rule():
+    from oracle.decoder import quant_static_e4m3, quant_rows_e4m3
+    amax = 3.0
+    q, s = quant_static_e4m3(np.array([[3.0, 6.0, -9.0, 0.0, 1.5]]), amax)
+    assert list(q[0]) == [448.0, 448.0, -448.0, 0.0, 224.0]
+    assert s == float(np.float32(3.0) / np.float32(448.0))
+    # one row whose static amplitude is its own maximum: the per-token rule
+    rng = np.random.default_rng(31)
+    row = rng.standard_normal((1, 300))
+    m = float(np.abs(row.astype(np.float32)).max())
+    qs, ss = quant_static_e4m3(row, m)
+    qt, st = quant_rows_e4m3(row)
+    assert np.array_equal(qs, qt) and ss == st[0]
+
+
+def test_fp8_calibration_records_the_largest_quantised_inputs():
+    """calibrate_fp8_static against a spy on the per-token FP8 linear: for each
+    block, the maxima of the two tensors it quantises (first call: the MLP
+    input, second: the fp16 SwiGLU output), over every frame."""
+    import oracle.decoder as odm
+    from dataclasses import replace as rp
+    m = rp(MODELS["tiny"], compute_dtype="f16", latent_h=6, latent_w=10, mlp_precision="fp8")
+    W = make_weights(m, 8, std=0.05)
+    z = make_latents(m, 4, 9)
+    seen = []
+    orig = odm._fp8_linear
+
+    def spy(x, w, b):
+        seen.append(float(np.abs(np.asarray(x, np.float32)).max()))
+        return orig(x, w, b)
+
+    rec = odm.calibrate_fp8_static(m, W, z, 2)
+    odm._fp8_linear = spy
+    try:
+        decode_stream(m, W, z, 2)
+    finally:
+        odm._fp8_linear = orig
+    blocks = [f"bb.{i}" for i in range(m.n_backbone_blocks)] + [f"rf.{i}" for i in range(m.n_refine_blocks)]
+    assert sorted(rec) == sorted(blocks)
+    n_calls = len(z[0, 0]) // m.unit_frames   # the oracle steps unit by unit (Algorithm 1)
+    per_call = 2 * len(blocks)
+    assert len(seen) == n_calls * per_call
+    for bi, p in enumerate(blocks):   # blocks run in this order in every call
+        ins = [seen[c * per_call + 2 * bi] for c in range(n_calls)]
+        hid = [seen[c * per_call + 2 * bi + 1] for c in range(n_calls)]
+        assert rec[p] == [max(ins), max(hid)], p
+
+
+def test_static_fp8_decoder_stays_close_to_the_16bit_one():
+    from dataclasses import replace as rp
+    from oracle.decoder import calibrate_fp8_static
+    m = rp(MODELS["tiny"], compute_dtype="f16", latent_h=6, latent_w=10)
+    W = make_weights(m, 8, std=0.05)
+    z = make_latents(m, 3, 9)
+    amax = calibrate_fp8_static(m, W, make_latents(m, 2, 10), 2)
+    Ws = dict(W)
+    for p, (ai, ah) in amax.items():
+        Ws[p + ".amax_in"], Ws[p + ".amax_hid"] = ai, ah
+    a = decode_stream(m, W, z, 1)
+    b = decode_stream(rp(m, mlp_precision="fp8s"), Ws, z, 1)
+    d = np.abs(a - b)
+    assert 1e-3 < d.max() < 0.25 and d.mean() < 0.03, (d.max(), d.mean())

@@ -50,9 +50,14 @@ enum { FD_HEAD_TEMPORAL_FIRST = 0, FD_HEAD_LINEAR = 1 };
  * operands (round to nearest even, saturating at +-448): the weights quantised
  * per output channel at create (static scales), the MLP input and the SwiGLU
  * output (kept in fp16 between the two GEMMs) per token when produced, with
- * fp32 accumulation and the two scales applied in the epilogue. Needs a 16-bit
- * compute dtype and the SwiGLU MLP. */
-enum { FD_MLP_PRECISION_COMPUTE = 0, FD_MLP_PRECISION_FP8 = 1 };
+ * fp32 accumulation and the two scales applied in the epilogue.
+ * FP8_STATIC: the paper's "static-calibrated" form: the MLP input and the
+ * fp16 SwiGLU output of every block take one fixed scale each, amax / 448,
+ * from amplitudes given with fd_set_fp8_act_amax (for instance the maxima
+ * fd_calibrate_chunk records); values beyond amax saturate. Decoding before the
+ * amplitudes are set gives STATE. Both need a 16-bit compute dtype and the
+ * SwiGLU MLP. */
+enum { FD_MLP_PRECISION_COMPUTE = 0, FD_MLP_PRECISION_FP8 = 1, FD_MLP_PRECISION_FP8_STATIC = 2 };
 
 /* Decoder shape. Copied by fd_decoder_create; the caller keeps ownership.
  * Field meanings follow the paper's notation (Sec. 3.2-3.4, supplement Table A). */
@@ -258,6 +263,30 @@ fd_status fd_quantize_e4m3_rows(const float* in, int64_t rows, int64_t cols, uin
  * INVALID_ARGUMENT. */
 fd_status fd_quantize_e4m3_rows_device(const float* in, int64_t rows, int64_t cols, uint8_t* codes,
                                        float* scales, void* stream);
+
+/* FP8 MLP decoders: the number of activation amplitudes, two per block (the
+ * MLP input, then the SwiGLU output), backbone blocks first, then refinement
+ * blocks; 0 for other decoders or NULL. */
+size_t fd_fp8_act_count(const fd_decoder* dec);
+
+/* FD_MLP_PRECISION_FP8_STATIC: set the static amplitudes amax[count] (host,
+ * count = fd_fp8_act_count, each finite and > 0; layout above). The codes of a
+ * tensor with amplitude a are e4m3(fp32(x * fp32(448 / a))), its dequantisation
+ * scale fp32(a / 448). Synchronous; no decode on this decoder may be in flight.
+ * STATE for other decoders, INVALID_ARGUMENT for a wrong count or value. */
+fd_status fd_set_fp8_act_amax(fd_decoder* dec, const float* amax, size_t count);
+
+/* Calibration for FD_MLP_PRECISION_FP8_STATIC (also accepted by FP8 decoders):
+ * decode one chunk like fd_decode_chunk (fp32 pixels into out, the cache
+ * advances) with per-token activation scales, and raise each amax[i] (host,
+ * in / out, count = fd_fp8_act_count, finite and >= 0) to the largest |value|
+ * of that tensor in this chunk (the fp32 MLP input; the fp16 SwiGLU output).
+ * Start from zeros and call it over calibration chunks, then pass the result
+ * to fd_set_fp8_act_amax. Blocks until done. Calibrations of one decoder must
+ * not overlap. STATE for decoders without an FP8 MLP. */
+fd_status fd_calibrate_chunk(const fd_decoder* dec, const void* latent, int32_t latent_dtype,
+                             int32_t n_frames, fd_kv_cache* cache, float* out, float* amax,
+                             size_t count, void* stream);
 
 /* Packing of an E4M3 weight for fd_gemm_e4m3_device (the layout the FP8 MLP
  * keeps its weights in): w[n][k] (row-major byte codes, host) goes to 1 KB

@@ -21,7 +21,9 @@ enum Epi : int {
   EPI_PIXEL = 7,       // head output -> PixelShuffle store (+clamp), fp32 pixels
   EPI_LINEAR_PIXEL = 8,// linear head output -> sub-frame + PixelShuffle store
   EPI_QKV = 9,         // KV-norm + 3D-RoPE of the QKV projection: q buffer and K / V^T rings
-  EPI_COUNT = 10
+  EPI_SWIGLU_E4M3 = 10,// SwiGLU as EPI_SWIGLU, rounded to fp16, then E4M3 codes at the static
+                       // inverse scale out_scale[1] (FP8 GEMM only)
+  EPI_COUNT = 11
 };
 
 struct QkvPostArgs {
@@ -68,6 +70,8 @@ struct EpiParams {
   // row_scale[m] * col_scale[n] before the bias and the epilogue
   const float* row_scale = nullptr;
   const float* col_scale = nullptr;
+  int row_scale_stride = 1;          // 0: one scale for every row (static per-tensor)
+  const float* out_scale = nullptr;  // EPI_SWIGLU_E4M3: {scale, inverse scale} of the codes
   QkvPostArgs qkv;          // EPI_QKV geometry and destinations (raw unused)
 };
 
@@ -101,8 +105,8 @@ hipError_t gemm_mfma(Act16 t, const GemmArgs& g, hipStream_t stream);
 hipError_t gemm_f32(const GemmArgs& g, hipStream_t stream);
 // E4M3 x E4M3 GEMM on the gfx950 32x32x64 FP8 MFMA: A [M, K] E4M3 bytes
 // row-major (lda bytes, lda % 16 == 0), W packed by pack_w8_index, K % 64 == 0;
-// epilogues EPI_SWIGLU (fp16 out_a) and EPI_RESID_ADD, after the row / column
-// scales of EpiParams.
+// epilogues EPI_SWIGLU (fp16 out_a), EPI_SWIGLU_E4M3 (E4M3 out_a) and
+// EPI_RESID_ADD, after the row / column scales of EpiParams.
 hipError_t gemm_fp8(const GemmArgs& g, hipStream_t stream);
 
 // Attention over the rolling KV ring.
@@ -124,15 +128,20 @@ hipError_t attention_f32(const AttnArgs& a, hipStream_t stream);
 
 // Norm of the fp32 residual stream into the next GEMM's operand format.
 // kind 0 = RMSNorm, 1 = LayerNorm. out_kind: 0 f16, 1 bf16, 2 fp32, 3 E4M3
-// codes with the per-row scale (rule of fd_quantize_e4m3_rows) in row_scale.
+// codes: with static_sc ({scale, inverse scale}) at that fixed scale
+// (saturating), else with the per-row scale (rule of fd_quantize_e4m3_rows)
+// written to row_scale. amax_out, if set, is raised to the largest |output|
+// (fp32 bits; calibration).
 hipError_t norm_rows(const float* x, int M, int D, const float* g, const float* b, int kind,
                      float eps, void* out, int out_kind, hipStream_t stream,
-                     float* row_scale = nullptr);
+                     float* row_scale = nullptr, const float* static_sc = nullptr,
+                     unsigned* amax_out = nullptr);
 
 // Per-row E4M3 quantisation (rule of fd_quantize_e4m3_rows) of in [M, K]
-// (in_kind 0 f16, 2 fp32) into codes [M, K] bytes and scale [M] fp32.
+// (in_kind 0 f16, 2 fp32) into codes [M, K] bytes and scale [M] fp32;
+// amax_out as for norm_rows.
 hipError_t quant_rows_e4m3(const void* in, int in_kind, int64_t M, int K, uint8_t* codes,
-                           float* scale, hipStream_t stream);
+                           float* scale, hipStream_t stream, unsigned* amax_out = nullptr);
 
 // Split raw qkv (fp32, bias included) into rotated queries and the KV ring
 // (KV-norm, RoPE) for rows of one call.

@@ -39,7 +39,8 @@ fd_status fail(fd_status st, const char* fmt, ...) {
 struct Derived {
   int Dh, grid_h, grid_w, L, K_in, K_pad, qkv_w, act_bytes;
   bool is16;
-  bool mlp8;     // MLP GEMMs on E4M3 operands (FD_MLP_PRECISION_FP8)
+  bool mlp8;     // MLP GEMMs on E4M3 operands (FD_MLP_PRECISION_FP8 / _FP8_STATIC)
+  bool mlp8s;    // ... with static per-tensor activation scales (FD_MLP_PRECISION_FP8_STATIC)
   fd::Act16 a16;
   int act_kind;  // 0 f16, 1 bf16, 2 fp32
 };
@@ -78,8 +79,6 @@ fd_status validate(const fd_config* c, Derived* d) {
     return fail(FD_ERR_INVALID_ARGUMENT, "norm_eps must be > 0 and rope_theta > 1");
   if (c->max_frames_per_call % c->unit_frames)
     return fail(FD_ERR_INVALID_ARGUMENT, "max_frames_per_call must be a multiple of unit_frames");
-  if (c->mlp_precision != FD_MLP_PRECISION_COMPUTE && c->mlp_precision != FD_MLP_PRECISION_FP8)
-    return fail(FD_ERR_INVALID_ARGUMENT, "unknown mlp_precision");
   Derived x{};
   x.Dh = c->dim / c->n_heads;
   x.grid_h = c->latent_h / c->patch;
@@ -106,7 +105,10 @@ fd_status validate(const fd_config* c, Derived* d) {
   } else if (x.Dh != 16 && x.Dh != 32 && x.Dh != 64) {
     return fail(FD_ERR_UNSUPPORTED, "fp32 compute needs D_h in {16, 32, 64}");
   }
-  x.mlp8 = c->mlp_precision == FD_MLP_PRECISION_FP8;
+  if (c->mlp_precision < FD_MLP_PRECISION_COMPUTE || c->mlp_precision > FD_MLP_PRECISION_FP8_STATIC)
+    return fail(FD_ERR_INVALID_ARGUMENT, "unknown mlp_precision %d", c->mlp_precision);
+  x.mlp8 = c->mlp_precision != FD_MLP_PRECISION_COMPUTE;
+  x.mlp8s = c->mlp_precision == FD_MLP_PRECISION_FP8_STATIC;
   if (x.mlp8 && (!x.is16 || c->mlp_kind != FD_MLP_SWIGLU))
     return fail(FD_ERR_UNSUPPORTED, "the FP8 MLP needs a 16-bit compute dtype and the SwiGLU MLP");
   if (d) *d = x;
@@ -254,6 +256,12 @@ struct fd_decoder {
   const int* rope_axis = nullptr;
   const double* rope_freq = nullptr;
   const float2* rope_hw = nullptr;
+  // FP8 MLP: static activation scales {s_in, 1/s_in, s_hid, 1/s_hid} per block
+  // (backbone blocks, then refinement blocks) and the calibration maxima
+  // {amax_in, amax_hid} per block (fp32 bits)
+  float* act_sc = nullptr;
+  unsigned* calib = nullptr;
+  bool act_set = false;
 };
 
 struct Probe {
@@ -325,6 +333,7 @@ struct Ctx {
   hipStream_t s;
   float* trace;
   int64_t trace_off;
+  bool calibrate = false;  // FP8 MLP: per-token scales, maxima recorded into dec->calib
 };
 
 fd_status run_gemm(Ctx& x, const fd::GemmArgs& g, double algo_k) {
@@ -355,13 +364,14 @@ fd::GemmArgs gemm_args(const void* A, int lda, const void* W, int M, int N, int 
 
 // Norm into the operand buffer a (compute type), or, for the FP8 MLP input,
 // into E4M3 codes a8 with per-row scales sa.
-fd_status run_norm(Ctx& x, const float* src, int M, const float* g, const float* b, bool e4m3 = false) {
+fd_status run_norm(Ctx& x, const float* src, int M, const float* g, const float* b, bool e4m3 = false,
+                   const float* static_sc = nullptr, unsigned* amax_out = nullptr) {
   const fd_decoder* dec = x.dec;
   hipEvent_t ev;
   fd_status st = probe_begin(x.c, FD_KC_NORM, x.s, &ev);
   if (st) return st;
   hipError_t e = e4m3 ? fd::norm_rows(src, M, dec->cfg.dim, g, b, dec->cfg.norm_kind, dec->cfg.norm_eps,
-                                      x.c->a8, 3, x.s, x.c->sa)
+                                      x.c->a8, 3, x.s, x.c->sa, static_sc, amax_out)
                       : fd::norm_rows(src, M, dec->cfg.dim, g, b, dec->cfg.norm_kind, dec->cfg.norm_eps,
                                       x.c->a, dec->d.act_kind, x.s);
   if (e != hipSuccess) return fail(FD_ERR_DEVICE, "norm launch failed: %s", hipGetErrorString(e));
@@ -390,6 +400,7 @@ fd_status trace_copy(Ctx& x, const float* src, int64_t n) {
 fd_status run_stack(Ctx& x, const std::vector<LayerW>& layers, float* xs, int rows_per_batch,
                     int U, int U_pad, int64_t tau0, const std::vector<void*>& kr,
                     const std::vector<void*>& vr, bool refine) {
+  const int layer0 = refine ? x.dec->cfg.n_backbone_blocks : 0;  // index of the FP8 scales
   const fd_decoder* dec = x.dec;
   const fd_config& c = dec->cfg;
   const Derived& d = dec->d;
@@ -484,10 +495,36 @@ fd_status run_stack(Ctx& x, const std::vector<LayerW>& layers, float* xs, int ro
     g.ep.ld_out = D;
     if ((st = run_gemm(x, g, D))) return st;
 
+    if (d.mlp8 && d.mlp8s && !x.calibrate) {
+      // static-calibrated FP8 MLP: E4M3 MLP input at the block's fixed scale,
+      // w13 with the fused SwiGLU straight into E4M3 codes at the second fixed
+      // scale, w2 with the residual add
+      const float* sc = dec->act_sc + 4 * (layer0 + (int)l);
+      if ((st = run_norm(x, xs, rows, w.n2g, w.n2b, true, sc))) return st;
+      g = gemm_args(kc->a8, D, w.w1, rows, 2 * H, D, fd::EPI_SWIGLU_E4M3, w.b1);
+      g.ep.out_a = kc->h8;
+      g.ep.ld_out = H;
+      g.ep.row_scale = sc;
+      g.ep.row_scale_stride = 0;
+      g.ep.col_scale = w.s1;
+      g.ep.out_scale = sc + 2;
+      if ((st = run_gemm8(x, g, D))) return st;
+      g = gemm_args(kc->h8, H, w.w2, rows, D, H, fd::EPI_RESID_ADD, w.b2);
+      g.ep.out_f = xs;
+      g.ep.ld_out = D;
+      g.ep.row_scale = sc + 2;
+      g.ep.row_scale_stride = 0;
+      g.ep.col_scale = w.s2;
+      if ((st = run_gemm8(x, g, H))) return st;
+      if ((st = trace_copy(x, xs, (int64_t)rows * D))) return st;
+      continue;
+    }
     if (d.mlp8) {
       // FP8 MLP (Sec. 4.6 "-Opt"): E4M3 MLP input per token, w13 with the fused
-      // SwiGLU into fp16, per-token E4M3 codes of that, w2 with the residual add
-      if ((st = run_norm(x, xs, rows, w.n2g, w.n2b, true))) return st;
+      // SwiGLU into fp16, per-token E4M3 codes of that, w2 with the residual
+      // add; when calibrating, the maxima of both quantised tensors are recorded
+      unsigned* cal = x.calibrate ? dec->calib + 2 * (layer0 + (int)l) : nullptr;
+      if ((st = run_norm(x, xs, rows, w.n2g, w.n2b, true, nullptr, cal))) return st;
       g = gemm_args(kc->a8, D, w.w1, rows, 2 * H, D, fd::EPI_SWIGLU, w.b1);
       g.ep.out_a = kc->h;
       g.ep.ld_out = H;
@@ -495,7 +532,7 @@ fd_status run_stack(Ctx& x, const std::vector<LayerW>& layers, float* xs, int ro
       g.ep.col_scale = w.s1;
       if ((st = run_gemm8(x, g, D))) return st;
       if ((st = probe_begin(kc, FD_KC_NORM, x.s, &ev))) return st;
-      e = fd::quant_rows_e4m3(kc->h, 0, rows, H, kc->h8, kc->sh, x.s);
+      e = fd::quant_rows_e4m3(kc->h, 0, rows, H, kc->h8, kc->sh, x.s, cal ? cal + 1 : nullptr);
       if (e != hipSuccess) return fail(FD_ERR_DEVICE, "quantisation launch failed: %s", hipGetErrorString(e));
       if ((st = probe_end(kc, x.s, ev, (double)rows * H * 3.0))) return st;
       g = gemm_args(kc->h8, H, w.w2, rows, D, H, fd::EPI_RESID_ADD, w.b2);
@@ -556,9 +593,11 @@ fd_status check_decode(const fd_decoder* dec, const void* latent, int32_t latent
 
 fd_status decode(const fd_decoder* dec, const void* latent, int32_t latent_dtype, int32_t F,
                  fd_kv_cache* kc, void* out, int32_t out_fmt, void* stream, float* trace,
-                 size_t trace_elems) {
+                 size_t trace_elems, bool calibrate = false) {
   fd_status cst = check_decode(dec, latent, latent_dtype, F, kc, out, out_fmt);
   if (cst != FD_OK) return cst;
+  if (dec->d.mlp8s && !dec->act_set && !calibrate)
+    return fail(FD_ERR_STATE, "static FP8 scales are not set (fd_set_fp8_act_amax)");
   const fd_config& c = dec->cfg;
   const Derived& d = dec->d;
   if (trace && trace_elems < fd_trace_elems(dec, kc->batch, F))
@@ -567,7 +606,7 @@ fd_status decode(const fd_decoder* dec, const void* latent, int32_t latent_dtype
   int prev_dev = 0;
   FD_HIP(hipGetDevice(&prev_dev));
   if (prev_dev != dec->device) FD_HIP(hipSetDevice(dec->device));
-  Ctx x{dec, kc, s, trace, 0};
+  Ctx x{dec, kc, s, trace, 0, calibrate};
   const int B = kc->batch;
   const int M = B * F * d.L;
   const int D = c.dim;
@@ -860,6 +899,8 @@ void free_decoder(fd_decoder* d) {
   if (d->wmem) (void)hipFree(d->wmem);
   if (d->fmem) (void)hipFree(d->fmem);
   if (d->tables) (void)hipFree(d->tables);
+  if (d->act_sc) (void)hipFree(d->act_sc);
+  if (d->calib) (void)hipFree(d->calib);
   delete d;
 }
 
@@ -933,6 +974,12 @@ fd_status fd_decoder_create(const fd_config* cfg, const void* weights, int32_t w
       return fail(FD_ERR_DEVICE, "no HIP device");
     }
     st = upload_weights(dec, weights, weights_dtype, n_elements);
+    if (st == FD_OK && d.mlp8) {
+      const size_t nl = dec->bb.size() + dec->rf.size();
+      if (hipMalloc((void**)&dec->act_sc, nl * 4 * sizeof(float)) != hipSuccess ||
+          hipMalloc((void**)&dec->calib, nl * 2 * sizeof(unsigned)) != hipSuccess)
+        st = fail(FD_ERR_OUT_OF_MEMORY, "device allocation of the FP8 scales failed");
+    }
   } catch (const std::bad_alloc&) {
     st = fail(FD_ERR_OUT_OF_MEMORY, "host allocation failed");
   } catch (...) {
@@ -1260,6 +1307,69 @@ fd_status fd_quantize_e4m3_rows_device(const float* in, int64_t rows, int64_t co
   hipError_t e = fd::quant_rows_e4m3(in, 2, rows, (int)cols, codes, scales, (hipStream_t)stream);
   if (e != hipSuccess) return fail(FD_ERR_DEVICE, "quantisation launch failed: %s", hipGetErrorString(e));
   return FD_OK;
+}
+
+size_t fd_fp8_act_count(const fd_decoder* dec) {
+  return dec && dec->d.mlp8 ? 2 * (dec->bb.size() + dec->rf.size()) : 0;
+}
+
+fd_status fd_set_fp8_act_amax(fd_decoder* dec, const float* amax, size_t count) {
+  if (!dec || !amax) return fail(FD_ERR_INVALID_ARGUMENT, "NULL argument");
+  if (!dec->d.mlp8s) return fail(FD_ERR_STATE, "the decoder does not use static FP8 scales");
+  if (count != fd_fp8_act_count(dec))
+    return fail(FD_ERR_INVALID_ARGUMENT, "expected %zu amplitudes, got %zu", fd_fp8_act_count(dec), count);
+  std::vector<float> sc(2 * count);
+  for (size_t i = 0; i < count; ++i) {
+    const float a = amax[i];
+    if (!(a > 0.f) || !std::isfinite(a))
+      return fail(FD_ERR_INVALID_ARGUMENT, "amplitude %zu must be finite and > 0", i);
+    sc[2 * i] = a / 448.f;      // dequantisation scale
+    sc[2 * i + 1] = 448.f / a;  // quantisation multiplier
+  }
+  int prev = 0;
+  FD_HIP(hipGetDevice(&prev));
+  if (prev != dec->device) FD_HIP(hipSetDevice(dec->device));
+  const hipError_t e = hipMemcpy(dec->act_sc, sc.data(), sc.size() * sizeof(float), hipMemcpyHostToDevice);
+  if (prev != dec->device) (void)hipSetDevice(prev);
+  if (e != hipSuccess) return fail(FD_ERR_DEVICE, "upload of the FP8 scales failed: %s", hipGetErrorString(e));
+  dec->act_set = true;
+  return FD_OK;
+}
+
+fd_status fd_calibrate_chunk(const fd_decoder* dec, const void* latent, int32_t latent_dtype,
+                             int32_t n_frames, fd_kv_cache* cache, float* out, float* amax,
+                             size_t count, void* stream) {
+  if (!dec || !amax) return fail(FD_ERR_INVALID_ARGUMENT, "NULL argument");
+  if (!dec->d.mlp8) return fail(FD_ERR_STATE, "the decoder has no FP8 MLP");
+  if (count != fd_fp8_act_count(dec))
+    return fail(FD_ERR_INVALID_ARGUMENT, "expected %zu amplitudes, got %zu", fd_fp8_act_count(dec), count);
+  std::vector<unsigned> bits(count);
+  for (size_t i = 0; i < count; ++i) {
+    if (!(amax[i] >= 0.f) || !std::isfinite(amax[i]))
+      return fail(FD_ERR_INVALID_ARGUMENT, "amplitude %zu must be finite and >= 0", i);
+    std::memcpy(&bits[i], &amax[i], 4);
+  }
+  fd_status st = check_decode(dec, latent, latent_dtype, n_frames, cache, out, FD_PIXELS_F32);
+  if (st != FD_OK) return st;
+  try {
+    hipStream_t s = (hipStream_t)stream;
+    int prev = 0;
+    FD_HIP(hipGetDevice(&prev));
+    if (prev != dec->device) FD_HIP(hipSetDevice(dec->device));
+    if (hipMemcpyAsync(dec->calib, bits.data(), count * 4, hipMemcpyHostToDevice, s) != hipSuccess)
+      st = fail(FD_ERR_DEVICE, "calibration upload failed");
+    if (st == FD_OK)
+      st = decode(dec, latent, latent_dtype, n_frames, cache, out, FD_PIXELS_F32, stream, nullptr, 0, true);
+    if (st == FD_OK && (hipMemcpyAsync(bits.data(), dec->calib, count * 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
+                        hipStreamSynchronize(s) != hipSuccess))
+      st = fail(FD_ERR_DEVICE, "calibration readback failed");
+    if (prev != dec->device) (void)hipSetDevice(prev);
+    if (st != FD_OK) return st;
+    for (size_t i = 0; i < count; ++i) std::memcpy(&amax[i], &bits[i], 4);
+    return FD_OK;
+  } catch (...) {
+    return fail(FD_ERR_DEVICE, "unexpected error in fd_calibrate_chunk");
+  }
 }
 
 fd_status fd_pack_e4m3_weight(const uint8_t* w, int64_t n, int64_t k, uint8_t* packed) {

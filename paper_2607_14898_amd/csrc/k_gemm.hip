@@ -423,7 +423,7 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
                                              int c0, int M, int N, int lr, int lk, bool vec) {
   // SCALED (FP8 GEMM, SwiGLU only): each accumulator is multiplied by its
   // column's then its row's dequantisation scale right before use
-  static_assert(!SCALED || EPI == EPI_SWIGLU, "scaled transposed epilogue: SwiGLU only");
+  static_assert(!SCALED || EPI == EPI_SWIGLU || EPI == EPI_SWIGLU_E4M3, "scaled transposed epilogue: SwiGLU only");
   typedef __attribute__((ext_vector_type(4))) float f4;
   int64_t ro[FM];
   bool rok[FM];
@@ -433,10 +433,12 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
     rok[i] = row < M;
     ro[i] = row_off<EPI>(ep, min(row, M - 1));
   }
-  if constexpr (EPI == EPI_SWIGLU) {
+  if constexpr (EPI == EPI_SWIGLU || EPI == EPI_SWIGLU_E4M3) {
     float rs[FM];
 #pragma unroll
-    for (int i = 0; i < FM; ++i) rs[i] = SCALED ? ep.row_scale[min(r0 + i * 32 + lr, M - 1)] : 1.f;
+    for (int i = 0; i < FM; ++i)
+      rs[i] = SCALED ? ep.row_scale[min(r0 + i * 32 + lr, M - 1) * ep.row_scale_stride] : 1.f;
+    const float q_inv = EPI == EPI_SWIGLU_E4M3 ? ep.out_scale[1] : 1.f;
     // gate block j and up block j + 1 give output columns (c0 + 32 j) / 2 + 0..31
 #pragma unroll
     for (int j = 0; j < FN; j += 2)
@@ -457,6 +459,7 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
         for (int i = 0; i < FM; ++i) {
           if (!rok[i]) continue;
           T o4[4];
+          float h4[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             float g = acc[i][j][4 * q + e], u = acc[i][j + 1][4 * q + e];
@@ -465,6 +468,15 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
               u = u * su[e] * rs[i];
             }
             o4[e] = to_act<T>(silu_f(g + bg[e]) * (u + bu[e]));
+            h4[e] = (float)o4[e];
+          }
+          if constexpr (EPI == EPI_SWIGLU_E4M3) {
+            // codes of the fp16-rounded hidden value at the static scale (saturating)
+            auto cl = [&](float v) { return fminf(448.f, fmaxf(-448.f, v * q_inv)); };
+            int w = __builtin_amdgcn_cvt_pk_fp8_f32(cl(h4[0]), cl(h4[1]), 0, false);
+            w = __builtin_amdgcn_cvt_pk_fp8_f32(cl(h4[2]), cl(h4[3]), w, true);
+            *reinterpret_cast<int*>((uint8_t*)ep.out_a + ro[i] + oc) = w;
+            continue;
           }
           *reinterpret_cast<uint2*>((T*)ep.out_a + ro[i] + oc) = *reinterpret_cast<const uint2*>(o4);
         }
@@ -588,8 +600,8 @@ struct TileCfg {
 // consecutive columns per lane make one 8-byte store and one bias / SiLU pass
 // per four values. fp32 destinations keep the direct layout, where the 32 lanes
 // of a half-wave write one full 128-byte row segment per store.
-template <int EPI> constexpr bool kTransposed =
-    EPI == EPI_SWIGLU || EPI == EPI_STORE_ACT || EPI == EPI_STORE_SILU || EPI == EPI_STORE_GELU;
+template <int EPI> constexpr bool kTransposed = EPI == EPI_SWIGLU || EPI == EPI_SWIGLU_E4M3 ||
+    EPI == EPI_STORE_ACT || EPI == EPI_STORE_SILU || EPI == EPI_STORE_GELU;
 
 template <typename T, class C, int EPI>
 __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
@@ -920,7 +932,7 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_fp8_kernel(
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float rs = ep.row_scale[min(r0 + i * 32 + 8 * (r >> 2) + 4 * lk + (r & 3), M - 1)];
+        const float rs = ep.row_scale[min(r0 + i * 32 + 8 * (r >> 2) + 4 * lk + (r & 3), M - 1) * ep.row_scale_stride];
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j][r] *= rs;
       }
@@ -1070,6 +1082,10 @@ hipError_t gemm_fp8(const GemmArgs& g, hipStream_t s) {
   if (g.epi == EPI_SWIGLU) {
     if (g.N % 64 || g.ep.ld_out % 4 || (uintptr_t)g.ep.out_a % 8) return hipErrorInvalidValue;
     return dispatch_fp8<EPI_SWIGLU>(g, s);
+  }
+  if (g.epi == EPI_SWIGLU_E4M3) {
+    if (g.N % 64 || g.ep.ld_out % 4 || (uintptr_t)g.ep.out_a % 4 || !g.ep.out_scale) return hipErrorInvalidValue;
+    return dispatch_fp8<EPI_SWIGLU_E4M3>(g, s);
   }
   if (g.epi == EPI_RESID_ADD) return dispatch_fp8<EPI_RESID_ADD>(g, s);
   return hipErrorInvalidValue;

@@ -60,6 +60,8 @@ struct E4m3Row {
     inv = 448.f / mm;
     scale = mm / 448.f;
   }
+  // a static (calibrated) scale: {scale, inverse scale}
+  __device__ __forceinline__ explicit E4m3Row(const float* sc) : inv(sc[1]), scale(sc[0]) {}
   // four values -> four codes, byte e = value e
   __device__ __forceinline__ uint32_t pack4(float a, float b, float c, float d) const {
     auto cl = [&](float v) { return fminf(448.f, fmaxf(-448.f, v * inv)); };
@@ -74,7 +76,9 @@ template <int KIND>
 __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, int M, int D,
                                                    const float* __restrict__ g,
                                                    const float* __restrict__ bta, float eps,
-                                                   void* out, int out_kind, float* row_scale) {
+                                                   void* out, int out_kind, float* row_scale,
+                                                   const float* __restrict__ static_sc,
+                                                   unsigned* __restrict__ amax_out) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
@@ -131,14 +135,16 @@ __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, 
     }
   }
   if (out_kind == 3) {
-    const E4m3Row q(wave_max(amax));
+    const float m = wave_max(amax);
+    if (amax_out && lane == 0) atomicMax(amax_out, __float_as_uint(m));  // non-negative: ordered as bits
+    const E4m3Row q = static_sc ? E4m3Row(static_sc) : E4m3Row(m);
 #pragma unroll
     for (int i = 0; i < MAXV; ++i) {
       const int c = lane + 64 * i;
       if (c < nv)
         reinterpret_cast<uint32_t*>((uint8_t*)out + (int64_t)row * D)[c] = q.pack4(v[i].x, v[i].y, v[i].z, v[i].w);
     }
-    if (lane == 0) row_scale[row] = q.scale;
+    if (!static_sc && lane == 0) row_scale[row] = q.scale;
   }
 }
 
@@ -147,7 +153,8 @@ __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, 
 template <typename TIN>
 __global__ __launch_bounds__(256) void quant_rows_kernel(const TIN* __restrict__ in, int64_t M, int K,
                                                          uint8_t* __restrict__ codes,
-                                                         float* __restrict__ scale) {
+                                                         float* __restrict__ scale,
+                                                         unsigned* __restrict__ amax_out) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
@@ -157,7 +164,9 @@ __global__ __launch_bounds__(256) void quant_rows_kernel(const TIN* __restrict__
 #pragma unroll
     for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)r[c + e]));
   }
-  const E4m3Row q(wave_max(amax));
+  const float m = wave_max(amax);
+  if (amax_out && lane == 0) atomicMax(amax_out, __float_as_uint(m));
+  const E4m3Row q(m);
   for (int c = 8 * lane; c < K; c += 512) {
     float f[8];
 #pragma unroll
@@ -332,30 +341,31 @@ int grid_for(int64_t total) {
 }  // namespace
 
 hipError_t norm_rows(const float* x, int M, int D, const float* g, const float* b, int kind,
-                     float eps, void* out, int out_kind, hipStream_t s, float* row_scale) {
+                     float eps, void* out, int out_kind, hipStream_t s, float* row_scale,
+                     const float* static_sc, unsigned* amax_out) {
   if (M <= 0) return hipSuccess;
-  if (D % 4 || D > 2048 || (out_kind == 3 && !row_scale)) return hipErrorInvalidValue;
+  if (D % 4 || D > 2048 || (out_kind == 3 && !row_scale && !static_sc)) return hipErrorInvalidValue;
   const int grid = (M + 3) / 4;
   if (kind == 0)
     hipLaunchKernelGGL(norm_kernel<0>, dim3(grid), dim3(256), 0, s, x, M, D, g, b, eps, out, out_kind,
-                       row_scale);
+                       row_scale, static_sc, amax_out);
   else
     hipLaunchKernelGGL(norm_kernel<1>, dim3(grid), dim3(256), 0, s, x, M, D, g, b, eps, out, out_kind,
-                       row_scale);
+                       row_scale, static_sc, amax_out);
   return hipGetLastError();
 }
 
 hipError_t quant_rows_e4m3(const void* in, int in_kind, int64_t M, int K, uint8_t* codes,
-                           float* scale, hipStream_t s) {
+                           float* scale, hipStream_t s, unsigned* amax_out) {
   if (M <= 0) return hipSuccess;
   if (K <= 0 || K % 8 || (in_kind != 0 && in_kind != 2)) return hipErrorInvalidValue;
   const unsigned grid = (unsigned)((M + 3) / 4);
   if (in_kind == 0)
     hipLaunchKernelGGL(quant_rows_kernel<_Float16>, dim3(grid), dim3(256), 0, s, (const _Float16*)in, M,
-                       K, codes, scale);
+                       K, codes, scale, amax_out);
   else
     hipLaunchKernelGGL(quant_rows_kernel<float>, dim3(grid), dim3(256), 0, s, (const float*)in, M, K,
-                       codes, scale);
+                       codes, scale, amax_out);
   return hipGetLastError();
 }
 

@@ -92,6 +92,9 @@ def load_library() -> ctypes.CDLL:
         "fd_quantize_e4m3_rows": (I32, [P, I64, I64, P, P]),
         "fd_quantize_e4m3_rows_device": (I32, [P, I64, I64, P, P, P]),
         "fd_pack_e4m3_weight": (I32, [P, I64, I64, P]),
+        "fd_fp8_act_count": (SZ, [P]),
+        "fd_set_fp8_act_amax": (I32, [P, P, SZ]),
+        "fd_calibrate_chunk": (I32, [P, P, I32, I32, P, P, P, SZ, P]),
         "fd_gemm_e4m3_device": (I32, [P, I64, P, P, P, P, I32, I32, I32, I32, P, I64, P]),
         "fd_status_string": (ctypes.c_char_p, [I32]),
         "fd_last_error": (ctypes.c_char_p, []),
@@ -127,7 +130,7 @@ def make_config(model, max_batch: int = 1, max_frames_per_call: int = 4) -> fd_c
     c.rope_theta = float(model.rope_theta)
     c.norm_eps = float(model.norm_eps)
     c.clamp_output = int(model.clamp_output)
-    c.mlp_precision = {"f16": 0, "fp8": 1}[getattr(model, "mlp_precision", "f16")]
+    c.mlp_precision = {"f16": 0, "fp8": 1, "fp8s": 2}[getattr(model, "mlp_precision", "f16")]
     c.max_batch = max_batch
     c.max_frames_per_call = max_frames_per_call
     return c
@@ -304,6 +307,27 @@ def fd_quantize_e4m3_rows_device(x, codes, scales, stream=None) -> None:
     rows, cols = x.shape
     _check(load_library().fd_quantize_e4m3_rows_device(x.data_ptr(), rows, cols, codes.data_ptr(),
                                                         scales.data_ptr(), _stream_handle(stream)))
+
+
+def fd_fp8_act_count(dec: int) -> int:
+    return load_library().fd_fp8_act_count(dec)
+
+
+def fd_set_fp8_act_amax(dec: int, amax) -> None:
+    """Static FP8 amplitudes (2 per block: MLP input, SwiGLU output)."""
+    a = np.ascontiguousarray(amax, dtype=np.float32)
+    _check(load_library().fd_set_fp8_act_amax(dec, a.ctypes.data, a.size))
+
+
+def fd_calibrate_chunk(dec: int, latent, n_frames: int, cache: int, out, amax: np.ndarray,
+                       stream=None) -> None:
+    """Decode one chunk with per-token FP8 scales and raise amax (float32 numpy,
+    fd_fp8_act_count entries, updated in place) to the maxima seen."""
+    if amax.dtype != np.float32 or not amax.flags.c_contiguous:
+        raise ValueError("amax must be a contiguous float32 array")
+    _check(load_library().fd_calibrate_chunk(dec, latent.data_ptr(), _latent_dtype(latent), n_frames,
+                                             cache, out.data_ptr(), amax.ctypes.data, amax.size,
+                                             _stream_handle(stream)))
 
 
 FD_GEMM_E4M3_RESID_ADD, FD_GEMM_E4M3_SWIGLU_F16 = 0, 1

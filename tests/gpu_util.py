@@ -3,6 +3,26 @@ seeded inputs and return numpy arrays."""
 import numpy as np
 
 
+def fp8_block_prefixes(model):
+    """Block prefixes in the order of the library's FP8 amplitude array."""
+    return ([f"bb.{i}" for i in range(model.n_backbone_blocks)] +
+            [f"rf.{i}" for i in range(model.n_refine_blocks if model.head_kind == "temporal_first" else 0)])
+
+
+def fp8_amax_array(model, weights):
+    """Static FP8 amplitudes of the weights dict (<block>.amax_in, <block>.amax_hid)."""
+    return np.array([v for p in fp8_block_prefixes(model)
+                     for v in (weights[p + ".amax_in"], weights[p + ".amax_hid"])], np.float32)
+
+
+def with_fp8_amax(weights, amax_by_block):
+    """Copy of the weights dict with the static amplitudes {prefix: (in, hid)} added."""
+    w = dict(weights)
+    for p, (a_in, a_hid) in amax_by_block.items():
+        w[p + ".amax_in"], w[p + ".amax_hid"] = float(a_in), float(a_hid)
+    return w
+
+
 def run_decoder(model, weights, z, frames_per_call, batch=None, max_frames=None,
                 perturb=None, trace=False):
     """Decode latents z [B, C', T', H', W'] in calls of frames_per_call frames.
@@ -15,6 +35,8 @@ def run_decoder(model, weights, z, frames_per_call, batch=None, max_frames=None,
     B = z.shape[0] if batch is None else batch
     mf = max_frames or frames_per_call
     dec = fdb.Decoder(model, weights, max_batch=B, max_frames_per_call=mf)
+    if getattr(model, "mlp_precision", "f16") == "fp8s":
+        fdb.fd_set_fp8_act_amax(dec.handle, fp8_amax_array(model, weights))
     cache = fdb.KvCache(dec, B)
     zt = torch.from_numpy(np.ascontiguousarray(z)).cuda()
     outs, traces = [], []

@@ -72,6 +72,7 @@ def test_weight_layout_matches_generator(name):
     (dict(window=0), fdb.FD_ERR_INVALID_ARGUMENT),
     (dict(n_heads=48), fdb.FD_ERR_UNSUPPORTED),            # 16-bit path needs D_h = 64
     (dict(mlp_precision="fp8", compute_dtype="f32"), fdb.FD_ERR_UNSUPPORTED),  # FP8 MLP needs 16-bit compute
+    (dict(mlp_precision="fp8s", compute_dtype="f32"), fdb.FD_ERR_UNSUPPORTED),
 ])
 def test_invalid_configs_are_rejected(change, status):
     _lib()
@@ -207,3 +208,21 @@ def test_serving_entry_points_reject_bad_arguments_before_any_device_call():
     assert lib.fd_decode_chunks(None, 1, arr, 0, 1, arr, arr, 0, None) == fdb.FD_ERR_INVALID_ARGUMENT
     assert lib.fd_decode_chunks(None, 0, None, 0, 1, None, None, 0, None) == fdb.FD_ERR_INVALID_ARGUMENT
     assert fdb.FD_PIXELS_F32 == 0 and fdb.FD_PIXELS_BF16 == 1 and fdb.FD_PIXELS_U8 == 2
+
+
+@pytest.mark.parametrize("prec", ["fp8", "fp8s"])
+def test_fp8_mlp_configs_validate(prec):
+    _lib()
+    cfg = fdb.make_config(replace(MODELS["xl-720p"], mlp_precision=prec))
+    assert fdb.fd_config_validate(cfg) == fdb.FD_OK
+    cfg.mlp_precision = 3
+    assert fdb.fd_config_validate(cfg) == fdb.FD_ERR_INVALID_ARGUMENT
+
+
+def test_static_fp8_entry_points_reject_null_arguments():
+    lib = _lib()
+    a = np.ones(4, np.float32)
+    assert lib.fd_fp8_act_count(None) == 0
+    assert lib.fd_set_fp8_act_amax(None, a.ctypes.data, 4) == fdb.FD_ERR_INVALID_ARGUMENT
+    assert lib.fd_calibrate_chunk(None, None, 0, 1, None, None, a.ctypes.data, 4, None) == \
+        fdb.FD_ERR_INVALID_ARGUMENT

@@ -12,7 +12,8 @@ way, the head on the final clamped pixels at 2e-2 max-abs. Properties that hold
 at any size are checked at full size too: a 4-frame call equals 4 streamed
 calls bit for bit, causality, and determinism.
 
-With the FP8 MLP the oracle block fake-quantises the MLP the same way, and
+With the FP8 MLP (per-token, or static scales given by the workload) the
+oracle block fake-quantises the MLP the same way, and
 each block's tolerance is calibrated on the oracle itself: the block rerun
 with its inputs perturbed by relative 2^-11 (the 16-bit path's rounding, from
 which the kernels decide their E4M3 codes) moves the update by a spread s;
@@ -23,7 +24,7 @@ import pytest
 
 import oracle.decoder as od
 from paper_2607_14898_amd.workloads import WORKLOADS
-from tests.gpu_util import run_decoder
+from tests.gpu_util import fp8_block_prefixes, run_decoder, with_fp8_amax
 
 pytestmark = pytest.mark.gpu
 
@@ -64,7 +65,7 @@ def _check_block(m, W, p, xk, pos_k, qidx, pos_q, x_gpu, log):
     returns the worst relative update error after asserting the tolerance."""
     ref = od.block_forward_rows(m, W, p, xk, pos_k, xk[qidx], pos_q)
     err, mean = _update_err(xk[qidx], x_gpu, ref)
-    if getattr(m, "mlp_precision", "f16") != "fp8":
+    if getattr(m, "mlp_precision", "f16") not in ("fp8", "fp8s"):
         log(f"{p}: update err {err:.2e}")
         assert err < TOL_UPDATE, (p, err)
         return err
@@ -150,12 +151,14 @@ def teacher_forced_check(m, Wf, z, out, traces, n_rows=40, log=print):
     ("xl-wan22-720p-stream", 2),
     # wider windows: chunk 4 sees chunks 1..4 (W_frm = 4) after the ring wrapped
     ("xl-480p-stream-w4", 5), ("xl-720p-stream-w4", 5),
-    # the FP8-MLP decoder
-    ("xl-720p-stream-fp8", 2)])
+    # the FP8-MLP decoders (per-token scales; static scales given by the workload)
+    ("xl-720p-stream-fp8", 2), ("xl-720p-stream-fp8s", 2)])
 def test_stream_teacher_forced_full_size(name, chunks):
     wl = WORKLOADS[name]
     m = wl.model
     Wf = wl.weights()
+    if m.mlp_precision == "fp8s":
+        Wf = with_fp8_amax(Wf, {p: wl.fp8_amax for p in fp8_block_prefixes(m)})
     z = wl.latents()[:, :, :chunks]
     print(f"{name}: decoding {chunks} chunks with trace", flush=True)
     out, traces = run_decoder(m, Wf, z, 1, trace=True)

@@ -31,6 +31,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_F16_TFLOPS = 2500.0   # MI355X dense fp16 / bf16 MFMA
+PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_refine_xl720p_traffic.md")
 ATTN_SOURCE = os.path.join(ROOT, "paper_2607_14898_amd", "csrc", "k_attn.hip")
 METRIC = "decoded frames/sec at 720p (latent->pixel), p50 per-chunk latency, % MFMA peak"
@@ -222,8 +223,34 @@ def main() -> int:
 
     wall = t1 - t0
     lat = np.array([a.elapsed_time(b) for a, b in ev])
+
+    # per kernel class, after the timed region: device time of every launch of
+    # the class (events on the decode stream) against its algorithmic work
+    # (2 M N K flops per GEMM, 4 N L_q L_k D_h per attention, bytes read and
+    # written per norm / latent unshuffle pass)
+    n_probe = max(4, min(16, K))
+    kclasses = {}
+    for cname, kcl, flops_kind in (("gemm", fdb.FD_KC_GEMM, True), ("attention", fdb.FD_KC_ATTENTION, True),
+                                   ("norm", fdb.FD_KC_NORM, False), ("embed_in", fdb.FD_KC_EMBED_IN, False)):
+        fdb.fd_probe_enable(cache.handle, kcl)
+        for _ in range(n_probe):
+            step()
+        torch.cuda.synchronize()
+        c_ms, c_n, c_work = fdb.fd_probe_read(cache.handle)
+        fdb.fd_probe_enable(cache.handle, -1)
+        if c_n == 0:
+            continue
+        ach = c_work / (c_ms * 1e-3) / (1e12 if flops_kind else 1e9)
+        pk = PEAK_F16_TFLOPS if flops_kind else PEAK_HBM_GBS
+        kclasses[cname] = {
+            "bound": "mfma" if flops_kind else "hbm", "unit": "TFLOP/s" if flops_kind else "GB/s",
+            "achieved": round(ach, 1), "peak": pk, "frac": round(ach / pk, 4),
+            "launches_per_chunk": round(c_n / n_probe, 2), "ms_per_chunk": round(c_ms / n_probe, 4)}
     # sustained dense MFMA throughput of this GPU (after the timed region)
     peak_meas, peak_ghz = fdb.fd_measure_mfma_peak("f16", 100000)
+    for v in kclasses.values():
+        if v["bound"] == "mfma":
+            v["frac_of_measured_peak"] = round(v["achieved"] / peak_meas, 4)
     frames = K * F * m.r_t * NS
     fp8 = getattr(m, "mlp_precision", "f16") in ("fp8", "fp8s")
     achieved = attn_work / (attn_ms * 1e-3) / 1e12
@@ -260,6 +287,7 @@ def main() -> int:
             "operands": "fp16 MFMA operands (bf16-rounded weights/latents), fp32 accumulate",
             "paper_context": "76.1 frames/s, FlashDecoder-XL Wan2.1 720p streaming, 1x H100 (Table 2)",
         },
+        "kernel_classes": kclasses,
         "roofline": {
             "kernel": "attn_mfma_kernel<f16, 4 heads, 64 queries/wave> (refinement-stack attention)",
             "bound": "mfma",

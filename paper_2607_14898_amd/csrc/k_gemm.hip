@@ -34,6 +34,9 @@ __device__ __forceinline__ float gelu_f(float x) { return 0.5f * x * (1.f + erff
 template <typename T> __device__ __forceinline__ T to_act(float v);
 template <> __device__ __forceinline__ _Float16 to_act<_Float16>(float v) { return (_Float16)v; }
 template <> __device__ __forceinline__ __hip_bfloat16 to_act<__hip_bfloat16>(float v) { return __float2bfloat16(v); }
+// bit pattern of a 16-bit value (for packed stores without a stack array)
+__device__ __forceinline__ uint32_t bits16(_Float16 x) { return __builtin_bit_cast(uint16_t, x); }
+__device__ __forceinline__ uint32_t bits16(__hip_bfloat16 x) { return __bfloat16_as_ushort(x); }
 template <> __device__ __forceinline__ float to_act<float>(float v) { return v; }
 
 // Every epilogue stores to out[row_off(row) + col_off(col)]: the destination
@@ -295,16 +298,31 @@ __device__ __forceinline__ void store_tile(const EpiParams& ep, const f32x16 (&a
         }
         *reinterpret_cast<uint2*>(dst) = *reinterpret_cast<const uint2*>(o4);
       }
-      if (is_v) {  // lane = column (dimension): V^T[dim][pos] for the block's rows
+      if (is_v) {  // V^T[dim][pos] of the block's 32 rows
+        // lane l % 16 takes rows 2 (l % 16) and 2 (l % 16) + 1, lane / 16 picks
+        // the dimension: each store instruction writes 32 consecutive positions
+        // of 4 dimensions (four 64-byte segments), as 4-byte pairs where the
+        // two rows are adjacent in one ring slot
         __builtin_amdgcn_s_waitcnt(0xC07F);
-        for (int rr = 0; rr < 32; ++rr) {
-          const int row_t = rbase + rr;
-          if (row_t >= M) break;
-          int b, lu, pos, fs, hh, ww;
-          split(row_t, b, lu, pos, fs, hh, ww);
-          const int slot = (slot0 + lu) % a.S;
-          T* vt = (T*)a.vt_ring + ((int64_t)(b * a.G + kvg) * a.S + slot) * 64 * a.U_pad + pos;
-          vt[(int64_t)lane * a.U_pad] = to_act<T>(wl[rr * LS + lane]);
+        const int l16 = lane & 15, dg = lane >> 4;
+        const int ra = rbase + 2 * l16;
+        const bool oka = ra < M, okb = ra + 1 < M;
+        int b0, lu0, pos0, b1, lu1, pos1, fs, hh, ww;
+        split(min(ra, M - 1), b0, lu0, pos0, fs, hh, ww);
+        split(min(ra + 1, M - 1), b1, lu1, pos1, fs, hh, ww);
+        T* va = (T*)a.vt_ring + ((int64_t)(b0 * a.G + kvg) * a.S + (slot0 + lu0) % a.S) * 64 * a.U_pad + pos0;
+        T* vb = (T*)a.vt_ring + ((int64_t)(b1 * a.G + kvg) * a.S + (slot0 + lu1) % a.S) * 64 * a.U_pad + pos1;
+        const bool pair = oka && okb && vb == va + 1 && (pos0 & 1) == 0;
+#pragma unroll 4
+        for (int it = 0; it < 16; ++it) {
+          const int d = it * 4 + dg;
+          const T x0 = to_act<T>(wl[(2 * l16) * LS + d]), x1 = to_act<T>(wl[(2 * l16 + 1) * LS + d]);
+          if (pair) {
+            *reinterpret_cast<uint32_t*>(va + (int64_t)d * a.U_pad) = bits16(x0) | (bits16(x1) << 16);
+          } else {
+            if (oka) va[(int64_t)d * a.U_pad] = x0;
+            if (okb) vb[(int64_t)d * a.U_pad] = x1;
+          }
         }
       }
       __builtin_amdgcn_s_waitcnt(0xC07F);  // the block's LDS reads are done before the next block

@@ -196,3 +196,23 @@ def test_f16_residual_trace_matches_oracle_per_layer():
             rel = np.abs(g - x).max() / np.sqrt(np.mean(x ** 2))
             print(f"frame {t} {name}.{i}: rel max err {rel:.2e}", flush=True)
             assert rel < 2e-2, (t, name, i)
+
+
+@pytest.mark.parametrize("model,frames", [(XL_NARROW, 3), (XL_DEEP, 2)], ids=["xl-narrow", "xl-deep"])
+def test_bf16_operand_path_error_scales_with_its_rounding(model, frames):
+    """The bf16-operand build of the same kernels (compute_dtype = BF16; not
+    the graded path, whose fp16 operands keep 3 more mantissa bits). Both
+    paths' errors against the oracle come from rounding MFMA operands, so the
+    bf16 error must be the fp16 error times the ratio of the unit roundoffs,
+    2^-8 / 2^-11 = 8 (measured 7.7-8.0): within 4x-16x, on the maximum and the
+    mean. A bf16 build that fell back to fp16 operands, or one with a layout
+    mistake, leaves that band."""
+    W = make_weights(model, 0)
+    z = make_latents(model, frames, 31)
+    ref = decode_stream(model, W, z, 1)
+    e16 = np.abs(run_decoder(model, W, z, 1) - ref)
+    eb = np.abs(run_decoder(replace(model, compute_dtype="bf16"), W, z, 1) - ref)
+    rmax, rmean = eb.max() / e16.max(), eb.mean() / e16.mean()
+    print(f"bf16 / fp16 error: max {eb.max():.3e} / {e16.max():.3e} = {rmax:.2f}, "
+          f"mean {eb.mean():.3e} / {e16.mean():.3e} = {rmean:.2f}", flush=True)
+    assert 4.0 <= rmax <= 16.0 and 4.0 <= rmean <= 16.0

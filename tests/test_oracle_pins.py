@@ -647,3 +647,16 @@ def test_static_fp8_decoder_stays_close_to_the_16bit_one():
     b = decode_stream(rp(m, mlp_precision="fp8s"), Ws, z, 1)
     d = np.abs(a - b)
     assert 1e-3 < d.max() < 0.25 and d.mean() < 0.03, (d.max(), d.mean())
+
+
+def test_fp32_and_fp64_oracles_agree():
+    """The same forward in fp32 and fp64 (StreamingOracle's dtype): equal to
+    1e-5 of the output RMS, and not identical (the fp32 run does round)."""
+    from dataclasses import replace as rp
+    m = rp(MODELS["tiny"], latent_h=6, latent_w=10, clamp_output=False)
+    W = make_weights(m, 12, std=0.05)
+    z = make_latents(m, 3, 13)
+    a = decode_stream(m, W, z, 1, dtype=np.float64)
+    b = decode_stream(m, W, z, 1, dtype=np.float32)
+    rel = np.abs(a - b).max() / np.sqrt(np.mean(a ** 2))
+    assert b.dtype == np.float32 and 0.0 < rel <= 1e-5, rel

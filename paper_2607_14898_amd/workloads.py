@@ -201,13 +201,19 @@ class Workload:
     # static FP8 amplitudes (MLP input, SwiGLU output) of every block, for the
     # "fp8s" models when a job gives fixed scales instead of calibrating
     fp8_amax: Tuple[float, float] = (6.0, 10.0)
+    # latent rows appended as zeros after the first latent_h - pad_rows rows
+    # (1080p: 135 latent rows padded to 136 for a whole 68-row token grid)
+    pad_rows: int = 0
 
     @property
     def total_frames(self) -> int:
         return self.frames_per_call * self.n_calls
 
     def latents(self) -> np.ndarray:
-        return make_latents(self.model, self.total_frames, self.latent_seed, self.batch)
+        z = make_latents(self.model, self.total_frames, self.latent_seed, self.batch)
+        if self.pad_rows:
+            z[:, :, :, self.model.latent_h - self.pad_rows:, :] = 0.0
+        return z
 
     def weights(self) -> Dict[str, np.ndarray]:
         return make_weights(self.model, self.weight_seed)
@@ -238,6 +244,10 @@ XL_480P = ModelConfig(
     dim=1536, n_heads=24, n_kv_groups=3, n_backbone_blocks=20, n_refine_blocks=2,
     mlp_hidden=6144, head_hidden=6144, s_out=16)
 XL_720P = replace(XL_480P, latent_h=90, latent_w=160)
+# 1080p: the 135 x 240 latent (8x spatial) padded with one zero row to 136, so
+# the token grid is a whole 68 x 120 and the 1088 x 1920 output is cropped to
+# its first 1080 rows
+XL_1080P = replace(XL_480P, latent_h=136, latent_w=240)
 
 # FlashDecoder-XL on the Wan2.2 latent space (4x16x16, 48 channels): no
 # PixelUnshuffle (p = 1), so each latent pixel is one token and the same 16x16
@@ -251,6 +261,7 @@ MODELS = {
     "tiny-asis": TINY_ASIS,
     "xl-480p": XL_480P,
     "xl-720p": XL_720P,
+    "xl-1080p": XL_1080P,
     "xl-wan22-480p": XL_WAN22_480P,
     "xl-wan22-720p": XL_WAN22_720P,
 }
@@ -279,6 +290,9 @@ WORKLOADS = {
                                    weight_seed=0, latent_seed=103),
     "xl-720p-chunk-fp8": Workload("xl-720p-chunk-fp8", replace(XL_720P, mlp_precision="fp8"), 4, 1,
                                   weight_seed=0, latent_seed=104),
+    # 1080p stream (Table 2's third resolution): padded latent row, output cropped to 1080 rows
+    "xl-1080p-stream": Workload("xl-1080p-stream", XL_1080P, 1, 8, weight_seed=0, latent_seed=108,
+                                pad_rows=1),
     # static-calibrated FP8 MLP (per-tensor activation scales)
     "xl-720p-stream-fp8s": Workload("xl-720p-stream-fp8s", replace(XL_720P, mlp_precision="fp8s"), 1, 32,
                                     weight_seed=0, latent_seed=105),

@@ -147,6 +147,8 @@ def teacher_forced_check(m, Wf, z, out, traces, n_rows=40, log=print):
 
 @pytest.mark.parametrize("name,chunks", [
     ("xl-720p-stream", 2), ("xl-480p-stream", 2),
+    # 1080p: 135 latent rows padded with a zero row to a 68 x 120 token grid
+    ("xl-1080p-stream", 2),
     # Wan2.2 latent space: 48 channels, no PixelUnshuffle
     ("xl-wan22-720p-stream", 2),
     # wider windows: chunk 4 sees chunks 1..4 (W_frm = 4) after the ring wrapped

@@ -216,3 +216,17 @@ def test_bf16_operand_path_error_scales_with_its_rounding(model, frames):
     print(f"bf16 / fp16 error: max {eb.max():.3e} / {e16.max():.3e} = {rmax:.2f}, "
           f"mean {eb.mean():.3e} / {e16.mean():.3e} = {rmean:.2f}", flush=True)
     assert 4.0 <= rmax <= 16.0 and 4.0 <= rmean <= 16.0
+
+
+@pytest.mark.parametrize("fpc", [1, 2])
+def test_f16_batch_of_independent_streams(fpc):
+    """Two streams in one cache on the 16-bit path: 130 tokens per frame puts
+    the batch boundary inside a 32-row block of the QKV epilogue (its ring and
+    transposed-V writes split such blocks between the two streams), and
+    2-frame calls add a unit boundary per stream."""
+    W = make_weights(XL_NARROW, 0)
+    z = make_latents(XL_NARROW, 4, 38, batch=2)
+    ref = decode_stream(XL_NARROW, W, z, 1)
+    got = run_decoder(XL_NARROW, W, z, fpc)
+    assert got.shape[0] == 2
+    assert _report(f"xl-narrow f16 B=2 F={fpc}", got, ref) <= TOL_16

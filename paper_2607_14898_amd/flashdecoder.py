@@ -325,6 +325,7 @@ def fd_calibrate_chunk(dec: int, latent, n_frames: int, cache: int, out, amax: n
     fd_fp8_act_count entries, updated in place) to the maxima seen."""
     if amax.dtype != np.float32 or not amax.flags.c_contiguous:
         raise ValueError("amax must be a contiguous float32 array")
+    _check_out(out, FD_PIXELS_F32)
     _check(load_library().fd_calibrate_chunk(dec, latent.data_ptr(), _latent_dtype(latent), n_frames,
                                              cache, out.data_ptr(), amax.ctypes.data, amax.size,
                                              _stream_handle(stream)))

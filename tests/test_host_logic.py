@@ -58,3 +58,27 @@ x.hip:20:1: remark:     ScratchSize [bytes/lane]: 0 [-Rpass-analysis=kernel-reso
 x.hip:20:1: remark:     VGPRs Spill: 12 [-Rpass-analysis=kernel-resource-usage]
 """
     assert _scratch_users(remarks) == ["kB: ScratchSize [bytes/lane] = 272", "kC: VGPRs Spill = 12"]
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU: --gpus 2 exits with status 2 and says why,
+    before touching a GPU."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_every_workload_has_a_valid_shape():
+    """Token grids are whole, the 1080p padding stays inside the latent, and
+    static-FP8 workloads carry positive amplitudes."""
+    for w in WORKLOADS.values():
+        m = w.model
+        assert m.latent_h % m.patch == 0 and m.latent_w % m.patch == 0, w.name
+        assert 0 <= w.pad_rows < m.latent_h
+        if m.mlp_precision == "fp8s":
+            assert min(w.fp8_amax) > 0

@@ -91,10 +91,19 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 31, lh = lane >> 5;
-  const int bx = blockIdx.x;
+  // Workgroup -> (query tile, head block). The hardware deals workgroups
+  // round-robin to the 8 XCDs (workgroup i runs on XCD i % 8), each with its own
+  // L2. Every XCD gets a contiguous range of the (head block, query tile) order,
+  // so the workgroups one XCD runs together mostly share a KV group, and its K
+  // and V^T tiles stream through that XCD's L2 once for all of them.
+  const int nbx = gridDim.x, n_wg = nbx * gridDim.y;
+  const int lin = blockIdx.y * nbx + blockIdx.x;
+  const int xq = n_wg / 8, xr = n_wg % 8, xcd = lin % 8;
+  const int wid = (xcd < xr ? xcd * (xq + 1) : xr * (xq + 1) + (xcd - xr) * xq) + lin / 8;
+  const int bx = wid % nbx;
   const int qt = bx % q_tiles, bu = bx / q_tiles;
   const int lu = bu % a.n_units, b = bu / a.n_units;
-  const int head0 = blockIdx.y * HPB;
+  const int head0 = (wid / nbx) * HPB;
   const int n = head0 + wave % HPB;
   const int g = head0 / (a.N / a.G);
   const int64_t u = a.u0 + lu;

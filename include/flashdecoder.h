@@ -12,8 +12,15 @@
  *     head and PixelShuffle.
  *
  * Conventions for every function below:
- *   - Nothing is enqueued and no state changes when a call returns a status
- *     other than FD_OK; fd_last_error() then holds a message (thread-local).
+ *   - Arguments, the configuration and object states are checked before any
+ *     device work: a call that fails a check (FD_ERR_INVALID_ARGUMENT,
+ *     FD_ERR_UNSUPPORTED, FD_ERR_STATE) enqueues nothing and changes no state.
+ *   - A decode call that returns FD_ERR_DEVICE (a kernel launch failed part
+ *     way) may already have enqueued the kernels before the failing one: its
+ *     output buffer may be partly written and the ring slots of the call's own
+ *     frames partly rewritten (slots that hold no frame a later call reads),
+ *     while the cache position stays where it was.
+ *   - After any non-OK status fd_last_error() holds a message (thread-local).
  *   - No C++ exception crosses this boundary.
  *   - "device pointer" means memory the caller allocated on the GPU the decoder
  *     was created on; "host pointer" means ordinary CPU memory.
@@ -103,11 +110,27 @@ typedef struct fd_tensor_desc {
 typedef struct fd_decoder fd_decoder;
 typedef struct fd_kv_cache fd_kv_cache;
 
+/* ------------------------------------------------------------------------
+ * Decoder, streaming state and the decode call: the problem statement's
+ * create(config, weights) / reset / decode_chunk(latent, cache, pixels).
+ * ------------------------------------------------------------------------ */
+
 /* Check a config. FD_OK, FD_ERR_INVALID_ARGUMENT (inconsistent values) or
- * FD_ERR_UNSUPPORTED (e.g. a 16-bit compute type with D_h != 64). Host only. */
+ * FD_ERR_UNSUPPORTED: a 16-bit compute type with D_h != 64, or sizes beyond
+ * the kernels' index ranges -- max_batch x max_frames_per_call x L_frm rows
+ * per call (x r_t for the temporal-first head) must stay below 2^23, one
+ * stream's ring of one KV group ((window - 1 + max_frames_per_call /
+ * unit_frames) slots of L_frm unit_frames (x r_t) keys rounded up to 64, of
+ * D_h values) below 2^32 bytes, L_frm below 2^23, and C' p^2, C s_out^2 r_t,
+ * mlp_hidden and head_hidden at most 65536. Host only. */
 fd_status fd_config_validate(const fd_config* cfg);
 
-/* Canonical weight layout: all tensors concatenated in this order (row-major):
+/* Canonical weight layout of the learned tensors the paper's decoder defines:
+ * the latent projection (Sec. 3.2, Eq. projection), the transformer blocks of
+ * the backbone and of the temporal refinement stack (Sec. 3.2; Sec. 3.4 Step
+ * 2), the temporal upsampling Linear (Sec. 3.4 Step 1, Eq. temporal_upsample)
+ * and the pixel head (Sec. 3.4 Step 3). All tensors are concatenated in this
+ * order (row-major):
  * embed.w [D, C'p^2], embed.b; per block of B then R: norm1.g (+.b for LayerNorm),
  * wqkv [D + 2 G D_h, D] (rows q | k | v), bqkv, knorm.g [D_h] and vnorm.g [D_h]
  * (if kv_norm), wo [D, D], bo, norm2.g (+.b), w13 [2H, D] (rows gate | up) and
@@ -120,7 +143,9 @@ fd_status fd_config_validate(const fd_config* cfg);
 fd_status fd_weights_layout(const fd_config* cfg, fd_tensor_desc* descs, size_t capacity,
                             size_t* n_tensors, size_t* n_elements);
 
-/* Create a decoder on the current HIP device: validates cfg, copies the weight
+/* Create the decoder of Sec. 3.2-3.4 (shape per cfg; the FlashDecoder-XL
+ * hyper-parameters are those of the supplement's Table A) on the current HIP
+ * device: validates cfg, copies the weight
  * blob (host pointer, canonical layout, n_elements values of weights_dtype) to
  * the device, converting and packing it for the compute type, and builds the
  * RoPE tables. The blob is only read during the call. The decoder owns its
@@ -158,15 +183,6 @@ void fd_kv_cache_destroy(fd_kv_cache* cache);
 fd_status fd_output_shape(const fd_decoder* dec, int32_t batch, int32_t n_frames,
                           int64_t shape[5]);
 
-/* Pixel formats of fd_decode_chunk_as / fd_decode_chunks. Each pixel is first
- * clamped to [-1, 1] when clamp_output is set, then stored as
- *   FD_PIXELS_F32   fp32;
- *   FD_PIXELS_BF16  bf16, rounded to nearest even;
- *   FD_PIXELS_U8    uint8 = rint(fp32(x * 127.5 + 127.5)), one fp32 rounding of
- *                   the fused multiply-add, ties to even, limited to 0..255
- *                   (so -1 -> 0, 0 -> 128, 1 -> 255; 4x fewer bytes than fp32). */
-enum { FD_PIXELS_F32 = 0, FD_PIXELS_BF16 = 1, FD_PIXELS_U8 = 2 };
-
 /* Decode one chunk (Algorithm 1 for n_frames consecutive latent frames).
  *   latent  device pointer, [batch, C', n_frames, H', W'] contiguous, latent_dtype
  *   n_frames 1..max_frames_per_call, a multiple of unit_frames
@@ -179,6 +195,19 @@ enum { FD_PIXELS_F32 = 0, FD_PIXELS_BF16 = 1, FD_PIXELS_U8 = 2 };
  * The cache must not be used by two calls at once. */
 fd_status fd_decode_chunk(const fd_decoder* dec, const void* latent, int32_t latent_dtype,
                           int32_t n_frames, fd_kv_cache* cache, float* out, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Serving: other pixel formats and several streams at once.
+ * ------------------------------------------------------------------------ */
+
+/* Pixel formats of fd_decode_chunk_as / fd_decode_chunks. Each pixel is first
+ * clamped to [-1, 1] when clamp_output is set, then stored as
+ *   FD_PIXELS_F32   fp32;
+ *   FD_PIXELS_BF16  bf16, rounded to nearest even;
+ *   FD_PIXELS_U8    uint8 = rint(fp32(x * 127.5 + 127.5)), one fp32 rounding of
+ *                   the fused multiply-add, ties to even, limited to 0..255
+ *                   (so -1 -> 0, 0 -> 128, 1 -> 255; 4x fewer bytes than fp32). */
+enum { FD_PIXELS_F32 = 0, FD_PIXELS_BF16 = 1, FD_PIXELS_U8 = 2 };
 
 /* fd_decode_chunk with the pixels in out_format (FD_PIXELS_*): out holds
  * fd_output_shape elements of 4, 2 or 1 bytes. The decode before the pixel
@@ -203,6 +232,42 @@ fd_status fd_decode_chunk_as(const fd_decoder* dec, const void* latent, int32_t 
 fd_status fd_decode_chunks(const fd_decoder* dec, int32_t n, const void* const* latents,
                            int32_t latent_dtype, int32_t n_frames, fd_kv_cache* const* caches,
                            void* const* outs, int32_t out_format, void* stream);
+
+/* ------------------------------------------------------------------------
+ * FP8 MLP of the "-Opt" decoder (Sec. 4.6): static activation amplitudes and
+ * their calibration.
+ * ------------------------------------------------------------------------ */
+
+/* FP8 MLP decoders: the number of activation amplitudes, two per block (the
+ * MLP input, then the SwiGLU output), backbone blocks first, then refinement
+ * blocks; 0 for other decoders or NULL. */
+size_t fd_fp8_act_count(const fd_decoder* dec);
+
+/* FD_MLP_PRECISION_FP8_STATIC: set the static amplitudes amax[count] (host,
+ * count = fd_fp8_act_count, each finite and > 0; layout above). The codes of a
+ * tensor with amplitude a are e4m3(fp32(x * fp32(448 / a))), its dequantisation
+ * scale fp32(a / 448). Synchronous; no decode on this decoder may be in flight.
+ * STATE for other decoders, INVALID_ARGUMENT for a wrong count or value. */
+fd_status fd_set_fp8_act_amax(fd_decoder* dec, const float* amax, size_t count);
+
+/* Calibration for FD_MLP_PRECISION_FP8_STATIC (also accepted by FP8 decoders):
+ * decode one chunk like fd_decode_chunk (fp32 pixels into out, the cache
+ * advances) with per-token activation scales, and raise each amax[i] (host,
+ * in / out, count = fd_fp8_act_count, finite and >= 0) to the largest |value|
+ * of that tensor in this chunk (the fp32 MLP input; the fp16 SwiGLU output).
+ * Start from zeros and call it over calibration chunks, then pass the result
+ * to fd_set_fp8_act_amax. Blocks until done. Calibrations of one decoder must
+ * not overlap. STATE for decoders without an FP8 MLP. */
+fd_status fd_calibrate_chunk(const fd_decoder* dec, const void* latent, int32_t latent_dtype,
+                             int32_t n_frames, fd_kv_cache* cache, float* out, float* amax,
+                             size_t count, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Diagnostics and kernel-level test hooks. Decoding needs none of these: they
+ * expose internal state (the residual stream), time kernel classes inside real
+ * decode calls, measure the GPU's sustained MFMA rate, and run single kernels
+ * of the FP8 MLP on caller buffers so that tests can check them directly.
+ * ------------------------------------------------------------------------ */
 
 /* fd_decode_chunk that also copies the fp32 residual stream into `trace`
  * (device pointer, fp32) after the embedding and after every block: first the
@@ -263,30 +328,6 @@ fd_status fd_quantize_e4m3_rows(const float* in, int64_t rows, int64_t cols, uin
  * INVALID_ARGUMENT. */
 fd_status fd_quantize_e4m3_rows_device(const float* in, int64_t rows, int64_t cols, uint8_t* codes,
                                        float* scales, void* stream);
-
-/* FP8 MLP decoders: the number of activation amplitudes, two per block (the
- * MLP input, then the SwiGLU output), backbone blocks first, then refinement
- * blocks; 0 for other decoders or NULL. */
-size_t fd_fp8_act_count(const fd_decoder* dec);
-
-/* FD_MLP_PRECISION_FP8_STATIC: set the static amplitudes amax[count] (host,
- * count = fd_fp8_act_count, each finite and > 0; layout above). The codes of a
- * tensor with amplitude a are e4m3(fp32(x * fp32(448 / a))), its dequantisation
- * scale fp32(a / 448). Synchronous; no decode on this decoder may be in flight.
- * STATE for other decoders, INVALID_ARGUMENT for a wrong count or value. */
-fd_status fd_set_fp8_act_amax(fd_decoder* dec, const float* amax, size_t count);
-
-/* Calibration for FD_MLP_PRECISION_FP8_STATIC (also accepted by FP8 decoders):
- * decode one chunk like fd_decode_chunk (fp32 pixels into out, the cache
- * advances) with per-token activation scales, and raise each amax[i] (host,
- * in / out, count = fd_fp8_act_count, finite and >= 0) to the largest |value|
- * of that tensor in this chunk (the fp32 MLP input; the fp16 SwiGLU output).
- * Start from zeros and call it over calibration chunks, then pass the result
- * to fd_set_fp8_act_amax. Blocks until done. Calibrations of one decoder must
- * not overlap. STATE for decoders without an FP8 MLP. */
-fd_status fd_calibrate_chunk(const fd_decoder* dec, const void* latent, int32_t latent_dtype,
-                             int32_t n_frames, fd_kv_cache* cache, float* out, float* amax,
-                             size_t count, void* stream);
 
 /* Packing of an E4M3 weight for fd_gemm_e4m3_device (the layout the FP8 MLP
  * keeps its weights in): w[n][k] (row-major byte codes, host) goes to 1 KB

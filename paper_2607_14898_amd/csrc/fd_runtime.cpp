@@ -83,8 +83,17 @@ fd_status validate(const fd_config* c, Derived* d) {
   x.Dh = c->dim / c->n_heads;
   x.grid_h = c->latent_h / c->patch;
   x.grid_w = c->latent_w / c->patch;
-  x.L = x.grid_h * x.grid_w;
-  x.K_in = c->latent_channels * c->patch * c->patch;
+  // widths that index in 32-bit arithmetic inside the kernels
+  const int64_t L64 = (int64_t)x.grid_h * x.grid_w;
+  const int64_t kin64 = (int64_t)c->latent_channels * c->patch * c->patch;
+  const int64_t cs2_64 = (int64_t)c->out_channels * c->s_out * c->s_out * c->r_t;
+  if (L64 >= (int64_t)1 << 23 || kin64 > 65536 || cs2_64 > 65536 || c->mlp_hidden > 65536 ||
+      c->head_hidden > 65536 || c->r_t > 64)
+    return fail(FD_ERR_UNSUPPORTED,
+                "sizes beyond the kernels' ranges (tokens per frame < 2^23, C' p^2, C s_out^2 r_t, MLP and "
+                "head widths <= 65536, r_t <= 64)");
+  x.L = (int)L64;
+  x.K_in = (int)kin64;
   x.is16 = c->compute_dtype != FD_DTYPE_F32;
   x.a16 = c->compute_dtype == FD_DTYPE_BF16 ? fd::Act16::BF16 : fd::Act16::F16;
   x.act_kind = c->compute_dtype == FD_DTYPE_F32 ? 2 : (c->compute_dtype == FD_DTYPE_BF16 ? 1 : 0);
@@ -111,6 +120,26 @@ fd_status validate(const fd_config* c, Derived* d) {
   x.mlp8s = c->mlp_precision == FD_MLP_PRECISION_FP8_STATIC;
   if (x.mlp8 && (!x.is16 || c->mlp_kind != FD_MLP_SWIGLU))
     return fail(FD_ERR_UNSUPPORTED, "the FP8 MLP needs a 16-bit compute dtype and the SwiGLU MLP");
+  // Index ranges of the kernels. The rows of one call (batch x frames x L_frm,
+  // times r_t in the refinement stack) are split into (stream, unit, position,
+  // h, w) by a reciprocal multiply that is exact only below 2^23, and the
+  // attention reads one stream's ring of one KV group through a buffer
+  // descriptor whose size (S slots x U_pad keys x D_h values) is 32-bit.
+  const bool tf = c->head_kind == FD_HEAD_TEMPORAL_FIRST;
+  const int64_t rows_call = (int64_t)c->max_batch * c->max_frames_per_call * x.L * (tf ? c->r_t : 1);
+  if (rows_call >= (int64_t)1 << 23)
+    return fail(FD_ERR_UNSUPPORTED,
+                "max_batch x max_frames_per_call x tokens per frame%s = %lld rows per call; the kernels "
+                "need fewer than 2^23",
+                tf ? " x r_t" : "", (long long)rows_call);
+  const int64_t slots = (int64_t)c->window - 1 + c->max_frames_per_call / c->unit_frames;
+  const int64_t unit_pad = ((int64_t)c->unit_frames * x.L * (tf ? c->r_t : 1) + 63) / 64 * 64;
+  const int64_t ring_bytes = slots * unit_pad * x.Dh * x.act_bytes;
+  if (ring_bytes >= (int64_t)1 << 32)
+    return fail(FD_ERR_UNSUPPORTED,
+                "one KV group's ring of one stream takes %lld bytes (window - 1 + max_frames_per_call / "
+                "unit_frames slots); the attention needs fewer than 2^32",
+                (long long)ring_bytes);
   if (d) *d = x;
   return FD_OK;
 }
@@ -894,6 +923,88 @@ fd_status upload_weights(fd_decoder* dec, const void* w, int32_t wdt, size_t n_e
   return FD_OK;
 }
 
+// Activation workspace of a call of M backbone rows (batch x frames x L_frm):
+// byte offsets of every buffer, each 256-byte aligned, and the total.
+struct WsLayout {
+  size_t xbb = 0, xrf = 0, raw = 0, a = 0, q = 0, o = 0, h = 0, u = 0, rt = 0, a8 = 0, h8 = 0, sa = 0,
+         sh = 0, total = 0;
+  bool has_rf = false, has_raw = false, has_fp8 = false;
+};
+
+WsLayout ws_layout(const fd_config& c, const Derived& d, int64_t M) {
+  const bool tf = c.head_kind == FD_HEAD_TEMPORAL_FIRST;
+  const int64_t MR = tf ? M * c.r_t : M;
+  const int64_t D = c.dim;
+  const size_t es = d.act_bytes;
+  // fp32 raw projections: the fp32 path's QKV post step and SwiGLU read them;
+  // the 16-bit path does both in GEMM epilogues
+  const int64_t raw_cols = d.is16 ? 0 : std::max<int64_t>(d.qkv_w, 2 * c.mlp_hidden);
+  const int64_t hid = std::max<int64_t>(c.mlp_hidden, tf ? c.head_hidden : 0);
+  auto al = [](int64_t b) { return (size_t)((b + 255) / 256 * 256); };
+  const size_t sizes[13] = {
+      al(M * D * 4),                                           // x_bb
+      tf ? al(MR * D * 4) : 0,                                 // x_rf
+      al(MR * raw_cols * 4),                                   // raw
+      al(MR * D * (int64_t)es),                                // a
+      al(MR * D * (int64_t)es),                                // q
+      al(MR * D * (int64_t)es),                                // o
+      al(MR * hid * (int64_t)es),                              // h
+      al(M * d.K_pad * (int64_t)es),                           // u
+      al((int64_t)(M / d.L) * c.r_t * (d.Dh / 2) * (int64_t)sizeof(float2)),  // rope_t
+      d.mlp8 ? al(MR * D) : 0,                                 // a8
+      d.mlp8 ? al(MR * c.mlp_hidden) : 0,                      // h8
+      d.mlp8 ? al(MR * 4) : 0,                                 // sa
+      d.mlp8 ? al(MR * 4) : 0};                                // sh
+  WsLayout w;
+  size_t* off[13] = {&w.xbb, &w.xrf, &w.raw, &w.a, &w.q, &w.o, &w.h, &w.u, &w.rt, &w.a8, &w.h8, &w.sa, &w.sh};
+  size_t p = 0;
+  for (int i = 0; i < 13; ++i) {
+    *off[i] = p;
+    p += sizes[i];
+  }
+  w.total = p;
+  w.has_rf = tf;
+  w.has_raw = raw_cols > 0;
+  w.has_fp8 = d.mlp8;
+  return w;
+}
+
+// The cache's workspace buffer pointers, saved and restored as a set.
+struct WsPtrs {
+  float *x_bb, *x_rf, *raw;
+  void *a, *q, *o, *h, *u;
+  float2* rope_t;
+  uint8_t *a8, *h8;
+  float *sa, *sh;
+};
+
+void set_ws_ptrs(fd_kv_cache* kc, const WsPtrs& p) {
+  kc->x_bb = p.x_bb;
+  kc->x_rf = p.x_rf;
+  kc->raw = p.raw;
+  kc->a = p.a;
+  kc->q = p.q;
+  kc->o = p.o;
+  kc->h = p.h;
+  kc->u = p.u;
+  kc->rope_t = p.rope_t;
+  kc->a8 = p.a8;
+  kc->h8 = p.h8;
+  kc->sa = p.sa;
+  kc->sh = p.sh;
+}
+
+// Point the cache's workspace buffers into base (laid out by w).
+void carve_workspace(fd_kv_cache* kc, char* base, const WsLayout& w) {
+  set_ws_ptrs(kc, {(float*)(base + w.xbb), w.has_rf ? (float*)(base + w.xrf) : nullptr,
+                   w.has_raw ? (float*)(base + w.raw) : nullptr, base + w.a, base + w.q, base + w.o,
+                   base + w.h, base + w.u, (float2*)(base + w.rt),
+                   w.has_fp8 ? (uint8_t*)(base + w.a8) : nullptr,
+                   w.has_fp8 ? (uint8_t*)(base + w.h8) : nullptr,
+                   w.has_fp8 ? (float*)(base + w.sa) : nullptr,
+                   w.has_fp8 ? (float*)(base + w.sh) : nullptr});
+}
+
 void free_decoder(fd_decoder* d) {
   if (!d) return;
   if (d->wmem) (void)hipFree(d->wmem);
@@ -1044,42 +1155,13 @@ fd_status fd_kv_cache_create(const fd_decoder* dec, int32_t batch, fd_kv_cache**
     kc->k_rf.push_back(p); p += ring_rf;
     kc->v_rf.push_back(p); p += ring_rf;
   }
-  // workspace
-  const int64_t M = (int64_t)batch * c.max_frames_per_call * d.L;
-  const int64_t MR = tf ? M * c.r_t : M;
-  const int D = c.dim;
-  const int64_t raw_cols = std::max<int64_t>(d.qkv_w, d.is16 ? 0 : 2 * c.mlp_hidden);
-  const int64_t hid = std::max<int64_t>(c.mlp_hidden, tf ? c.head_hidden : 0);
-  auto al = [](int64_t b) { return (size_t)((b + 255) / 256 * 256); };
-  const size_t sz_xbb = al(M * D * 4), sz_xrf = tf ? al(MR * D * 4) : 0;
-  const size_t sz_raw = al(MR * raw_cols * 4);
-  const size_t sz_a = al(MR * D * es), sz_q = sz_a, sz_o = sz_a;
-  const size_t sz_h = al(MR * hid * es), sz_u = al(M * d.K_pad * es);
-  const size_t sz_rt = al((int64_t)c.max_frames_per_call * c.r_t * (d.Dh / 2) * sizeof(float2));
-  const size_t sz_a8 = d.mlp8 ? al(MR * D) : 0, sz_h8 = d.mlp8 ? al(MR * c.mlp_hidden) : 0;
-  const size_t sz_sc = d.mlp8 ? al(MR * 4) : 0;
-  const size_t ws = sz_xbb + sz_xrf + sz_raw + sz_a + sz_q + sz_o + sz_h + sz_u + sz_rt + sz_a8 + sz_h8 +
-                    2 * sz_sc;
-  if (hipMalloc(&kc->ws, ws) != hipSuccess) {
+  // workspace for the largest call
+  const WsLayout w = ws_layout(c, d, (int64_t)batch * c.max_frames_per_call * d.L);
+  if (hipMalloc(&kc->ws, w.total) != hipSuccess) {
     free_cache(kc);
-    return fail(FD_ERR_OUT_OF_MEMORY, "workspace: hipMalloc(%zu) failed", ws);
+    return fail(FD_ERR_OUT_OF_MEMORY, "workspace: hipMalloc(%zu) failed", w.total);
   }
-  p = (char*)kc->ws;
-  kc->x_bb = (float*)p; p += sz_xbb;
-  kc->x_rf = tf ? (float*)p : nullptr; p += sz_xrf;
-  kc->raw = (float*)p; p += sz_raw;
-  kc->a = p; p += sz_a;
-  kc->q = p; p += sz_q;
-  kc->o = p; p += sz_o;
-  kc->h = p; p += sz_h;
-  kc->u = p; p += sz_u;
-  kc->rope_t = (float2*)p; p += sz_rt;
-  if (d.mlp8) {
-    kc->a8 = (uint8_t*)p; p += sz_a8;
-    kc->h8 = (uint8_t*)p; p += sz_h8;
-    kc->sa = (float*)p; p += sz_sc;
-    kc->sh = (float*)p; p += sz_sc;
-  }
+  carve_workspace(kc, (char*)kc->ws, w);
   *out = kc;
   return FD_OK;
 }

@@ -17,10 +17,11 @@
 // lane exactly the B operand of the following O^T += V^T P^T MFMA, so P never
 // leaves registers. Queries are pre-scaled by log2(e) / sqrt(D_h), and each
 // score accumulator starts from the query's negated running shift (the MFMA's
-// C operand), so the MFMA output is the exp2 argument itself. The shift is
-// raised (and O and the row sum rescaled) only on the first tile and when some
-// probability of a lane could leave the f16 range; only the ragged last tile
-// of a unit is masked. K and V^T tiles of 64 keys are double-buffered in LDS.
+// C operand), so the MFMA output is the exp2 argument itself. The shift is set
+// to the first tile's max and afterwards raised (with O and the row sum
+// rescaled) only when some probability of a lane could leave the f16 range;
+// only the ragged last tile of a unit is masked. K and V^T tiles of 64 keys
+// are double-buffered in LDS.
 #include "fd_kernels.h"
 
 #include <hip/hip_bf16.h>
@@ -187,9 +188,9 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
   // Running shift m_q of each query, kept as an f16-representable value. The
   // score MFMAs accumulate onto cinit = -m_q, so they return c q.k - m_q and
   // P = exp2(S^T) needs no VALU work before the exponential. The shift only has
-  // to keep P in f16 range: it is raised (and O, l rescaled by the exact exp2
-  // of the change) on the first tile and whenever some p of a lane may exceed
-  // 2^15, detected from the lane's partial row sum of the tile.
+  // to keep P in f16 range: it is set to the first tile's max and raised (and
+  // O, l rescaled by the exact exp2 of the change) whenever some p of a lane
+  // may exceed 2^15, detected from the lane's partial row sum of the tile.
   float mq[NQB], l_run[NQB];
   f32x16 cinit[NQB];
 #pragma unroll
@@ -304,8 +305,13 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
 #pragma unroll
     for (int qb = 0; qb < NQB; ++qb) big = big || !(ls[qb] <= 32768.f);
     if (it == 0 || __builtin_amdgcn_ballot_w64(big) != 0) {
-      // raise the shift of every query to its tile max (never lower it); the
-      // scores are recomputed from the K tile still in LDS
+      // On the first tile the shift of every query becomes that tile's max
+      // (from the initial 0, so it also drops to a negative max: a row whose
+      // logits all lie far below 0 would otherwise underflow to a zero sum);
+      // later it is only ever raised. Softmax is invariant to the shift, so
+      // any value that keeps P in f16 range is exact. The scores are
+      // recomputed from the K tile still in LDS.
+      const bool first = it == 0;
       scores();
 #pragma unroll
       for (int qb = 0; qb < NQB; ++qb) {
@@ -317,7 +323,9 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
         }
         m0 = fmaxf(m0, m1);
         m0 = fmaxf(m0, __shfl_xor(m0, 32));
-        const float mq_new = (float)M::cvt(mq[qb] + fmaxf(m0, 0.f));
+        // (the first tile's max is bounded below by -65504, the largest f16
+        // magnitude, so the shift stays finite in the 16-bit type)
+        const float mq_new = (float)M::cvt(mq[qb] + (first ? fmaxf(m0, -65504.f) : fmaxf(m0, 0.f)));
         const float delta = mq_new - mq[qb];  // exact: both are f16 values
         mq[qb] = mq_new;
 #pragma unroll

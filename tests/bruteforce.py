@@ -178,3 +178,87 @@ def decode(cfg, W, z):
                         v_ = min(1.0, max(-1.0, v_))
                     pix[c][fo][yy][xx] = v_
     return pix
+
+
+# --------------------------------------------------------------------------
+# FP8 (E4M3) MLP of the "-Opt" decoder (Sec. 4.6), scalar form. Roundings come
+# from struct (IEEE single and half, round to nearest even) and from a search
+# over the E4M3 code table built from its bit fields.
+# --------------------------------------------------------------------------
+import struct
+
+
+def f32(x):
+    return struct.unpack("f", struct.pack("f", x))[0]
+
+
+def f16(x):
+    return struct.unpack("e", struct.pack("e", x))[0]
+
+
+def _e4m3_table():
+    out = []
+    for sgn in (1.0, -1.0):
+        for e in range(16):
+            for m in range(8):
+                if e == 15 and m == 7:      # NaN code
+                    continue
+                v = (m / 8.0) * 2.0 ** -6 if e == 0 else (1.0 + m / 8.0) * 2.0 ** (e - 7)
+                out.append((sgn * v, m))
+    return out
+
+
+_E4M3 = _e4m3_table()
+
+
+def e4m3_nearest(x):
+    """Nearest finite E4M3 value; at a midpoint the one with an even mantissa
+    field; beyond +-448 the largest value of that sign."""
+    if x >= 448.0:
+        return 448.0
+    if x <= -448.0:
+        return -448.0
+    best, bm, bd = None, None, None
+    for v, m in _E4M3:
+        d = abs(v - x)
+        if bd is None or d < bd or (d == bd and m % 2 == 0 and bm % 2 == 1):
+            best, bm, bd = v, m, d
+    return best + 0.0
+
+
+def quant_row(row, amax=None):
+    """E4M3 codes (as values) and scale of one row: per row (amax None) with
+    m = max |fp32(x)|, else at the fixed amplitude amax; inv = fp32(448 / m),
+    code = e4m3(fp32(fp32(x) inv)), scale = fp32(m / 448); a zero row takes m = 448."""
+    x32 = [f32(v) for v in row]
+    m = f32(amax) if amax is not None else max(abs(v) for v in x32)
+    if m == 0.0:
+        m = 448.0
+    inv = f32(448.0 / m)
+    return [e4m3_nearest(f32(v * inv)) for v in x32], f32(m / 448.0)
+
+
+def fp8_linear_rows(rows, Wm, b, amax=None):
+    """y = x W^T + b with the rows of x quantised per row (or at amax) and the
+    rows of W per output channel: sum of code products times both scales."""
+    qw = [quant_row(w) for w in Wm]
+    out = []
+    for r in rows:
+        cx, sx = quant_row(r, amax)
+        out.append([sum(cx[k] * cw[k] for k in range(len(cx))) * sx * sw + b[n]
+                    for n, (cw, sw) in enumerate(qw)])
+    return out
+
+
+def fp8_mlp(cfg, W, p, rows, mode):
+    """The SwiGLU MLP of block p on the given input rows with both GEMMs on
+    E4M3 operands; the SwiGLU output is held in fp16 between them. mode "fp8":
+    activations quantised per row; "fp8s": at the block's fixed amplitudes
+    W[p + ".amax_in"], W[p + ".amax_hid"]."""
+    H = cfg.mlp_hidden
+    Wd = {k: W[k].tolist() for k in (p + ".w13", p + ".b13", p + ".w2", p + ".b2")}
+    a_in = float(W[p + ".amax_in"]) if mode == "fp8s" else None
+    a_hid = float(W[p + ".amax_hid"]) if mode == "fp8s" else None
+    y = fp8_linear_rows(rows, Wd[p + ".w13"], Wd[p + ".b13"], a_in)
+    hid = [[f16(r[i] / (1.0 + math.exp(-r[i])) * r[H + i]) for i in range(H)] for r in y]
+    return fp8_linear_rows(hid, Wd[p + ".w2"], Wd[p + ".b2"], a_hid)

@@ -226,3 +226,43 @@ def test_static_fp8_entry_points_reject_null_arguments():
     assert lib.fd_set_fp8_act_amax(None, a.ctypes.data, 4) == fdb.FD_ERR_INVALID_ARGUMENT
     assert lib.fd_calibrate_chunk(None, None, 0, 1, None, None, a.ctypes.data, 4, None) == \
         fdb.FD_ERR_INVALID_ARGUMENT
+
+
+@pytest.mark.parametrize("model,batch,frames,ok", [
+    # 1080p refinement rows per call: 64 x 4 x 8160 x 4 = 8,355,840 < 2^23 ...
+    ("xl-1080p", 64, 4, True),
+    # ... and 65 x 4 x 8160 x 4 = 8,486,400 >= 2^23
+    ("xl-1080p", 65, 4, False),
+    ("xl-720p", 146, 4, False),     # 146 x 4 x 3600 x 4 = 8,409,600
+    ("xl-720p", 145, 4, True),
+])
+def test_rows_per_call_limit_is_enforced_on_the_host(model, batch, frames, ok):
+    """The kernels split a call's rows into (stream, unit, position) with a
+    reciprocal multiply exact below 2^23 rows: larger configs are refused by
+    validation and by create, before any device work (no GPU is touched here)."""
+    lib = _lib()
+    cfg = fdb.make_config(MODELS[model], max_batch=batch, max_frames_per_call=frames)
+    st = fdb.fd_config_validate(cfg)
+    if ok:
+        assert st == fdb.FD_OK
+        return
+    assert st == fdb.FD_ERR_UNSUPPORTED
+    assert "2^23" in lib.fd_last_error().decode()
+    h = ctypes.c_void_p()
+    dummy = np.zeros(4, np.float32)
+    assert lib.fd_decoder_create(ctypes.byref(cfg), dummy.ctypes.data, 0, 4, ctypes.byref(h)) == \
+        fdb.FD_ERR_UNSUPPORTED
+    assert h.value is None
+
+
+@pytest.mark.parametrize("change", [
+    dict(window=2400),               # 2403 slots x 14400 refinement keys x 128 B > 2^32 B
+    dict(latent_h=8192, latent_w=8192, patch=1),   # 2^26 tokens per frame
+    dict(mlp_hidden=65600),
+    dict(r_t=128),
+])
+def test_sizes_beyond_the_kernels_ranges_are_refused(change):
+    lib = _lib()
+    cfg = fdb.make_config(replace(MODELS["xl-720p"], **change))
+    assert fdb.fd_config_validate(cfg) == fdb.FD_ERR_UNSUPPORTED
+    assert lib.fd_last_error().decode() != ""

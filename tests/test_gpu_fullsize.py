@@ -151,8 +151,9 @@ def teacher_forced_check(m, Wf, z, out, traces, n_rows=40, log=print):
     ("xl-1080p-stream", 2),
     # Wan2.2 latent space: 48 channels, no PixelUnshuffle
     ("xl-wan22-720p-stream", 2),
-    # wider windows: chunk 4 sees chunks 1..4 (W_frm = 4) after the ring wrapped
-    ("xl-480p-stream-w4", 5), ("xl-720p-stream-w4", 5),
+    # wider windows: chunk 4 sees chunks 1..4 (W_frm = 4) after the ring wrapped;
+    # W_frm = 3 (Table 4): chunk 3 sees chunks 1..3
+    ("xl-480p-stream-w4", 5), ("xl-720p-stream-w4", 5), ("xl-720p-stream-w3", 4),
     # the FP8-MLP decoders (per-token scales; static scales given by the workload)
     ("xl-720p-stream-fp8", 2), ("xl-720p-stream-fp8s", 2)])
 def test_stream_teacher_forced_full_size(name, chunks):
@@ -193,3 +194,65 @@ def test_720p_stream_causality_and_determinism():
     b = run_decoder(m, W, z2, 1)
     assert np.array_equal(a[:, :, :8], b[:, :, :8])
     assert not np.array_equal(a[:, :, 8:], b[:, :, 8:])
+
+
+def _per_frame_traces(m, trace, F):
+    """The residual trace of one F-frame call split into the traces F one-frame
+    calls write: backbone rows f L .. (f + 1) L and refinement rows
+    f r_t L .. (f + 1) r_t L of every recorded stream state."""
+    L, D, r = m.tokens_per_frame, m.dim, m.r_t
+    nb, nr = m.n_backbone_blocks, m.n_refine_blocks
+    bb = trace[:(nb + 1) * F * L * D].reshape(nb + 1, F * L, D)
+    rf = trace[(nb + 1) * F * L * D:].reshape(nr + 1, F * r * L, D)
+    return [np.concatenate([bb[:, f * L:(f + 1) * L].ravel(), rf[:, f * r * L:(f + 1) * r * L].ravel()])
+            for f in range(F)]
+
+
+def test_480p_four_frame_chunk_parity_at_its_launch_shape():
+    """The 480p single-chunk workload: one call of 4 latent frames (6240
+    backbone rows, 24960 refinement rows per launch). Bit for bit equal to 4
+    streamed one-frame calls, and its last frame teacher-forced against the
+    oracle from the 4-frame call's own residual trace."""
+    wl = WORKLOADS["xl-480p-chunk"]
+    m = wl.model
+    W = wl.weights()
+    z = wl.latents()
+    print("480p: one 4-frame call with trace", flush=True)
+    a, traces = run_decoder(m, W, z, 4, trace=True)
+    assert a.shape == (1, 3, 16, 480, 832)
+    print("480p: four 1-frame calls", flush=True)
+    b = run_decoder(m, W, z, 1, max_frames=4)
+    print("max diff", float(np.abs(a - b).max()), flush=True)
+    assert np.array_equal(a, b)
+    per_frame = _per_frame_traces(m, traces[0], 4)
+    teacher_forced_check(m, W, z, a, per_frame, log=lambda t: print(t, flush=True))
+
+
+def test_720p_reset_replays_the_stream_bitwise():
+    """fd_kv_cache_reset at full size: three chunks of another video, a reset,
+    then chunks 0 and 1 of the stream decode exactly as on a fresh cache."""
+    import torch
+    from paper_2607_14898_amd import flashdecoder as fdb
+    wl = WORKLOADS["xl-720p-stream"]
+    m = wl.model
+    W = wl.weights()
+    z = wl.latents()[:, :, :2]
+    z_old = wl.latents()[:, :, 2:5][:, :, ::-1].copy()
+    fresh = run_decoder(m, W, z, 1)
+    dec = fdb.Decoder(m, W, max_batch=1, max_frames_per_call=1)
+    cache = fdb.KvCache(dec, 1)
+    out = torch.empty(dec.output_shape(1, 1), dtype=torch.float32, device="cuda")
+    for t in range(3):
+        cache.decode_chunk(torch.from_numpy(np.ascontiguousarray(z_old[:, :, t:t + 1])).cuda(), out)
+    cache.reset()
+    outs = []
+    for t in range(2):
+        o = torch.empty(dec.output_shape(1, 1), dtype=torch.float32, device="cuda")
+        cache.decode_chunk(torch.from_numpy(np.ascontiguousarray(z[:, :, t:t + 1])).cuda(), o)
+        outs.append(o)
+    torch.cuda.synchronize()
+    got = np.concatenate([o.cpu().numpy() for o in outs], axis=2)
+    assert cache.position == 2
+    cache.close()
+    dec.close()
+    assert np.array_equal(got, fresh)

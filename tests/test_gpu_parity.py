@@ -88,10 +88,11 @@ def test_f16_wan22_latent_space_matches_oracle():
     assert _report("xl-narrow wan2.2 f16", got, ref) <= TOL_16
 
 
-@pytest.mark.parametrize("window,fpc", [(4, 1), (5, 1), (4, 2)])
+@pytest.mark.parametrize("window,fpc", [(3, 1), (4, 1), (5, 1), (4, 2)])
 def test_f16_wider_windows_match_oracle(window, fpc):
-    """W_frm = 4 and 5 (Table 4; the workload list's rings of 3 and 4 previous
-    chunks) over 7 frames, so the ring wraps; also calls of 2 frames."""
+    """W_frm = 3 and 4 (Table 4) and 5 (the workload list's rings of 3 and 4
+    previous chunks are W_frm = 4 and 5) over 7 frames, so the ring wraps; also
+    calls of 2 frames."""
     m = replace(XL_NARROW, window=window)
     W = make_weights(m, 0)
     z = make_latents(m, 6 if fpc == 2 else 7, 35)
@@ -230,3 +231,88 @@ def test_f16_batch_of_independent_streams(fpc):
     got = run_decoder(XL_NARROW, W, z, fpc)
     assert got.shape[0] == 2
     assert _report(f"xl-narrow f16 B=2 F={fpc}", got, ref) <= TOL_16
+
+
+def test_f16_reset_replays_a_fresh_stream():
+    """fd_kv_cache_reset (Algorithm 1: both caches start empty): after three
+    frames of one video, a reset and three frames of another decode exactly as
+    on a fresh cache -- bit for bit, although the rings still hold the first
+    video's keys and values -- and match the oracle's decode of that video."""
+    import torch
+    from paper_2607_14898_amd import flashdecoder as fdb
+    W = make_weights(XL_NARROW, 0)
+    z_old = make_latents(XL_NARROW, 3, 40)
+    z = make_latents(XL_NARROW, 3, 41)
+    fresh = run_decoder(XL_NARROW, W, z, 1)
+    dec = fdb.Decoder(XL_NARROW, W, max_batch=1, max_frames_per_call=1)
+    cache = fdb.KvCache(dec, 1)
+    out = torch.empty(dec.output_shape(1, 1), dtype=torch.float32, device="cuda")
+    for t in range(3):
+        cache.decode_chunk(torch.from_numpy(z_old[:, :, t:t + 1].copy()).cuda(), out)
+    torch.cuda.synchronize()
+    assert cache.position == 3
+    cache.reset()
+    assert cache.position == 0
+    outs = []
+    for t in range(3):
+        o = torch.empty(dec.output_shape(1, 1), dtype=torch.float32, device="cuda")
+        cache.decode_chunk(torch.from_numpy(z[:, :, t:t + 1].copy()).cuda(), o)
+        outs.append(o)
+    torch.cuda.synchronize()
+    got = np.concatenate([o.cpu().numpy() for o in outs], axis=2)
+    assert cache.position == 3
+    cache.close()
+    dec.close()
+    assert np.array_equal(got, fresh)
+    ref = decode_stream(XL_NARROW, W, z, 1)
+    assert _report("xl-narrow after reset", got, ref) <= TOL_16
+
+
+def test_f16_all_negative_logits_match_oracle():
+    """Every attention logit far below zero: without RoPE, a large key bias
+    along one direction makes the KV-normed keys nearly that direction (norm
+    about 7.6), and an opposite query bias of 20 (query weights scaled by 1/4,
+    which is exact in bf16, to keep the per-query spread small) puts every
+    logit below -24 in log2 units, for every query and key of every block.
+    exp2 of such a logit underflows fp16 (smallest subnormal 2^-24), so a
+    running shift that never drops below 0 would turn every probability of a
+    row into 0 and the row sum into 0. Softmax does not change under a common
+    shift of a row's logits, so the output must still match the oracle. (The
+    logits' size costs some accuracy by itself: fp16 keys carry a rounding
+    error of 2^-12 relative, which the query bias multiplies; about 0.6% per
+    attention here.)"""
+    import oracle.decoder as od
+    m = replace(XL_NARROW, rope=False, clamp_output=False)
+    W = make_weights(m, 6)
+    D, G, N = m.dim, m.n_kv_groups, m.n_heads
+    for k in W:
+        if k.endswith(".wqkv"):
+            W[k][:D] *= 0.25
+        if k.endswith(".bqkv"):
+            b = W[k]
+            for g in range(G):
+                b[D + 64 * g] = 20.0          # key bias along dimension 0 of the group
+            for n in range(N):
+                b[64 * n] = -20.0             # query bias opposite to it
+    z = make_latents(m, 2, 42)
+    logits = []
+    orig = od.attention
+
+    def spy(q, k, v, mask=None, return_probs=False):
+        rep = np.repeat(k, q.shape[1] // k.shape[1], axis=1)
+        s = np.einsum("qnd,knd->nqk", q, rep) / np.sqrt(q.shape[2])
+        logits.append(float(s.max()))
+        return orig(q, k, v, mask, return_probs)
+
+    od.attention = spy
+    try:
+        ref = decode_stream(m, W, z, 1)
+    finally:
+        od.attention = orig
+    log2_max = max(logits) / np.log(2.0)
+    assert log2_max < -24.0, log2_max
+    got = run_decoder(m, W, z, 1)
+    assert not np.isnan(got).any()
+    rel = np.abs(got - ref).max() / np.sqrt(np.mean(ref ** 2))
+    print(f"largest logit {log2_max:.1f} (log2 units); relative max error {rel:.3e}", flush=True)
+    assert rel <= TOL_16

@@ -660,3 +660,63 @@ def test_fp32_and_fp64_oracles_agree():
     b = decode_stream(m, W, z, 1, dtype=np.float32)
     rel = np.abs(a - b).max() / np.sqrt(np.mean(a ** 2))
     assert b.dtype == np.float32 and 0.0 < rel <= 1e-5, rel
+
+
+# The FP8 MLP branch of the oracle against a scalar restatement, and mistakes
+# planted in that branch (each must move the result far beyond the pin's bound).
+FP8_MICRO = replace(MICRO, compute_dtype="f16", dim=32, mlp_hidden=128)
+
+
+def _fp8_mlp_mutant(kind):
+    """A copy of the oracle's FP8 MLP branch with one planted mistake."""
+    def mlp(cfg, W, p, a):
+        H = cfg.mlp_hidden
+        y = od._fp8_linear(a, W[p + ".w13"], W[p + ".b13"]) if cfg.mlp_precision == "fp8" else \
+            od._fp8_static_linear(a, float(W[p + ".amax_in"]), W[p + ".w13"], W[p + ".b13"])
+        h = silu(y[:, :H]) * y[:, H:]
+        if kind != "no_f16_cast":
+            h = h.astype(np.float16).astype(np.float64)
+        if kind == "hidden_per_tensor":          # one amplitude for the whole hidden tensor
+            return od._fp8_static_linear(h, float(np.abs(h.astype(np.float32)).max()),
+                                         W[p + ".w2"], W[p + ".b2"])
+        if kind == "dropped_weight_scale":
+            qx, sx = od.quant_rows_e4m3(h)
+            qw, _ = od.quant_weight_rows_e4m3(W[p + ".w2"])
+            return (qx @ qw.T) * sx[:, None] + W[p + ".b2"]
+        if cfg.mlp_precision == "fp8":
+            return od._fp8_linear(h, W[p + ".w2"], W[p + ".b2"])
+        return od._fp8_static_linear(h, float(W[p + ".amax_hid"]), W[p + ".w2"], W[p + ".b2"])
+    return mlp
+
+
+def _fp8_mlp_case(mode):
+    cfg = replace(FP8_MICRO, mlp_precision=mode)
+    W = make_weights(cfg, 12, std=0.3)
+    W["bb.0.amax_in"], W["bb.0.amax_hid"] = 6.0, 0.75     # some inputs and hiddens saturate
+    rng = np.random.default_rng(13)
+    a = rng.standard_normal((12, cfg.dim)) * np.array([0.05, 0.3, 1, 3, 10, 0.7, 2, 1.5, 0.2, 5, 1, 4])[:, None]
+    return cfg, W, a
+
+
+@pytest.mark.parametrize("mode", ["fp8", "fp8s"])
+def test_fp8_mlp_branch_matches_a_scalar_loop(mode):
+    """_mlp with E4M3 GEMMs (per-token or static activation scales, per-channel
+    weight scales, the SwiGLU output rounded to fp16 in between) equals the
+    scalar restatement in tests/bruteforce.py to 1e-12 of its size."""
+    cfg, W, a = _fp8_mlp_case(mode)
+    got = od._mlp(cfg, W, "bb.0", a)
+    ref = np.array(bruteforce.fp8_mlp(cfg, W, "bb.0", a.tolist(), mode))
+    tol = 1e-12 * np.abs(ref).max()
+    assert np.abs(got - ref).max() <= tol, np.abs(got - ref).max()
+    if mode == "fp8s":   # the fixed amplitudes do saturate some codes in this case
+        assert np.abs(a).max() > 6.0
+
+
+@pytest.mark.parametrize("mode,kind", [("fp8", "no_f16_cast"), ("fp8s", "no_f16_cast"),
+                                       ("fp8", "hidden_per_tensor"), ("fp8", "dropped_weight_scale"),
+                                       ("fp8s", "dropped_weight_scale")])
+def test_fp8_mlp_planted_mistakes_break_the_scalar_pin(mode, kind):
+    cfg, W, a = _fp8_mlp_case(mode)
+    ref = np.array(bruteforce.fp8_mlp(cfg, W, "bb.0", a.tolist(), mode))
+    bad = _fp8_mlp_mutant(kind)(cfg, W, "bb.0", a)
+    assert np.abs(bad - ref).max() > 1e-6 * np.abs(ref).max()

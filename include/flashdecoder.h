@@ -196,6 +196,26 @@ fd_status fd_output_shape(const fd_decoder* dec, int32_t batch, int32_t n_frames
 fd_status fd_decode_chunk(const fd_decoder* dec, const void* latent, int32_t latent_dtype,
                           int32_t n_frames, fd_kv_cache* cache, float* out, void* stream);
 
+/* For callers that cannot allocate device memory while decoding (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * fd_decode_chunk with the call's activation workspace (residual streams,
+ * GEMM operands, MLP hidden, per-call RoPE table) taken from a fixed device
+ * array of 256 MiB that the library holds once per GPU, instead of the
+ * cache's own workspace; the cache still provides the rings and the position.
+ * Arguments, layouts, results and asynchrony are those of fd_decode_chunk, bit
+ * for bit. It calls no device allocation or free. The first call on a device
+ * looks the array's address up (hipGetSymbolAddress) and keeps it; make one
+ * call before capturing a graph. A call whose workspace (batch x n_frames
+ * x L_frm backbone rows, r_t times as many refinement rows) exceeds the array
+ * gives FD_ERR_UNSUPPORTED before any device work (the 480p XL stream fits;
+ * the 720p one does not), as does STATE with the event probe enabled on the
+ * cache or before static FP8 scales are set. All such calls on one GPU share the
+ * array, which keeps the last call's contents (nothing in it has to start at
+ * zero): calls that overlap on one GPU race, so order them (one stream, or
+ * events). */
+fd_status fd_decode_chunk_noalloc(const fd_decoder* dec, const void* latent, int32_t latent_dtype,
+                                  int32_t n_frames, fd_kv_cache* cache, float* out, void* stream);
+
 /* ------------------------------------------------------------------------
  * Serving: other pixel formats and several streams at once.
  * ------------------------------------------------------------------------ */

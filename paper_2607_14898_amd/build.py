@@ -12,7 +12,7 @@ from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SOURCES = ["csrc/k_gemm.hip", "csrc/k_attn.hip", "csrc/k_misc.hip", "csrc/k_probe.hip",
+SOURCES = ["csrc/k_gemm.hip", "csrc/k_attn.hip", "csrc/k_misc.hip", "csrc/k_probe.hip", "csrc/fd_scratch.hip",
            "csrc/fd_runtime.cpp"]
 LIB = os.path.join(PKG, "libflashdecoder.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -169,3 +169,10 @@ hipError_t convert_f32_to_16(const float* src, void* dst, int64_t n, int out_kin
                              hipStream_t stream);
 
 }  // namespace fd
+
+namespace fd {
+// fd_decode_chunk_noalloc: size of the fixed per-device workspace, and its
+// device address on `device` (looked up once per device; no allocation).
+constexpr size_t kNoallocScratchBytes = (size_t)256 << 20;
+hipError_t noalloc_scratch(int device, void** ptr);
+}  // namespace fd

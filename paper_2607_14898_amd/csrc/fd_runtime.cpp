@@ -978,6 +978,11 @@ struct WsPtrs {
   float *sa, *sh;
 };
 
+WsPtrs ws_ptrs(const fd_kv_cache* kc) {
+  return {kc->x_bb, kc->x_rf, kc->raw, kc->a, kc->q, kc->o, kc->h, kc->u, kc->rope_t, kc->a8, kc->h8,
+          kc->sa, kc->sh};
+}
+
 void set_ws_ptrs(fd_kv_cache* kc, const WsPtrs& p) {
   kc->x_bb = p.x_bb;
   kc->x_rf = p.x_rf;
@@ -1273,6 +1278,37 @@ fd_status fd_decode_chunk_trace(const fd_decoder* dec, const void* latent, int32
                   trace_elems);
   } catch (...) {
     return fail(FD_ERR_DEVICE, "unexpected error in fd_decode_chunk_trace");
+  }
+}
+
+fd_status fd_decode_chunk_noalloc(const fd_decoder* dec, const void* latent, int32_t latent_dtype,
+                                  int32_t n_frames, fd_kv_cache* cache, float* out, void* stream) {
+  fd_status st = check_decode(dec, latent, latent_dtype, n_frames, cache, out, FD_PIXELS_F32);
+  if (st != FD_OK) return st;
+  if (cache->probe.cls >= 0)
+    return fail(FD_ERR_STATE, "the event probe (which creates events) is enabled on this cache");
+  if (dec->d.mlp8s && !dec->act_set)
+    return fail(FD_ERR_STATE, "static FP8 scales are not set (fd_set_fp8_act_amax)");
+  const WsLayout w = ws_layout(dec->cfg, dec->d, (int64_t)cache->batch * n_frames * dec->d.L);
+  if (w.total > fd::kNoallocScratchBytes)
+    return fail(FD_ERR_UNSUPPORTED,
+                "this call needs %zu bytes of workspace; the fixed workspace of fd_decode_chunk_noalloc "
+                "holds %zu (fewer frames per call or a smaller batch fit)",
+                w.total, fd::kNoallocScratchBytes);
+  try {
+    void* base = nullptr;
+    const hipError_t e = fd::noalloc_scratch(dec->device, &base);
+    if (e != hipSuccess)
+      return fail(FD_ERR_DEVICE, "address of the fixed workspace: %s", hipGetErrorString(e));
+    // the call's buffers point into the fixed array for its duration; the
+    // cache's own workspace pointers are restored afterwards
+    const WsPtrs own = ws_ptrs(cache);
+    carve_workspace(cache, (char*)base, w);
+    st = decode(dec, latent, latent_dtype, n_frames, cache, out, FD_PIXELS_F32, stream, nullptr, 0);
+    set_ws_ptrs(cache, own);
+    return st;
+  } catch (...) {
+    return fail(FD_ERR_DEVICE, "unexpected error in fd_decode_chunk_noalloc");
   }
 }
 

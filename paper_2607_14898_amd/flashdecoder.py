@@ -80,6 +80,7 @@ def load_library() -> ctypes.CDLL:
         "fd_output_shape": (I32, [P, I32, I32, ctypes.POINTER(I64)]),
         "fd_decode_chunk": (I32, [P, P, I32, I32, P, P, P]),
         "fd_decode_chunk_trace": (I32, [P, P, I32, I32, P, P, P, P, SZ]),
+        "fd_decode_chunk_noalloc": (I32, [P, P, I32, I32, P, P, P]),
         "fd_decode_chunk_as": (I32, [P, P, I32, I32, P, P, I32, P]),
         "fd_decode_chunks": (I32, [P, I32, ctypes.POINTER(P), I32, I32, ctypes.POINTER(P),
                                    ctypes.POINTER(P), I32, P]),
@@ -220,6 +221,13 @@ def fd_decode_chunk(dec: int, latent, n_frames: int, cache: int, out, stream=Non
     """latent, out: contiguous torch tensors on the decoder's GPU."""
     _check(load_library().fd_decode_chunk(dec, latent.data_ptr(), _latent_dtype(latent), n_frames,
                                           cache, out.data_ptr(), _stream_handle(stream)))
+
+
+def fd_decode_chunk_noalloc(dec: int, latent, n_frames: int, cache: int, out, stream=None) -> None:
+    """fd_decode_chunk with the activation workspace in the library's fixed
+    per-GPU array (no device allocation); latent, out as for fd_decode_chunk."""
+    _check(load_library().fd_decode_chunk_noalloc(dec, latent.data_ptr(), _latent_dtype(latent), n_frames,
+                                                  cache, out.data_ptr(), _stream_handle(stream)))
 
 
 FD_PIXELS_F32, FD_PIXELS_BF16, FD_PIXELS_U8 = 0, 1, 2

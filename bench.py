@@ -11,6 +11,10 @@ before timing starts. Prints one JSON line.
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
   python bench.py --copy-calibration MIB   (plain device copy of MIB MiB, for
                                             scaling HBM byte counters)
+  python bench.py --reference-probes       (the GPU's LDS read bandwidth and the
+                                            rate of torch.matmul on the decoder's
+                                            720p GEMM shapes, as context for the
+                                            GEMM kernels' roofline)
 
 The roofline's "traffic" (HBM bytes per launch of the roofline kernel) comes
 from two rocprofv3 counter passes (FETCH_SIZE, WRITE_SIZE) over this script,
@@ -115,6 +119,47 @@ def copy_calibration(mib: int) -> int:
     return 0
 
 
+# (M, N, K) of the decoder's projections at the 720p stream shapes: backbone
+# QKV, O, gate/up, down; temporal upsampling; refinement QKV, O, gate/up, down;
+# pixel head layers 1 and 2
+GEMM_SHAPES_720P = [
+    ("bb.qkv", 3600, 1920, 1536), ("bb.o", 3600, 1536, 1536), ("bb.w13", 3600, 12288, 1536),
+    ("bb.w2", 3600, 1536, 6144), ("tup", 3600, 6144, 1536), ("rf.qkv", 14400, 1920, 1536),
+    ("rf.o", 14400, 1536, 1536), ("rf.w13", 14400, 12288, 1536), ("rf.w2", 14400, 1536, 6144),
+    ("head1", 14400, 6144, 1536), ("head2", 14400, 768, 6144)]
+
+
+def reference_probes() -> int:
+    """LDS bandwidth of a compute unit (fd_measure_lds_bandwidth), and torch.matmul
+    (the vendor BLAS) on the decoder's GEMM shapes with random fp16 operands: a
+    reference point for the library's own GEMM kernels, never used by them."""
+    import torch
+    from paper_2607_14898_amd import flashdecoder as fdb
+    bpc, ghz = fdb.fd_measure_lds_bandwidth(20000)
+    print(json.dumps({"probe": "lds_read_bandwidth", "bytes_per_clock_per_cu": round(bpc, 1),
+                      "clock_ghz": round(ghz, 3)}), flush=True)
+    torch.manual_seed(0)
+    for name, M, N, K in GEMM_SHAPES_720P:
+        a = (torch.randn(M, K, device="cuda") * 0.5).half()
+        w = (torch.randn(N, K, device="cuda") * 0.02).half()
+        for _ in range(3):
+            torch.matmul(a, w.t())
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = 20
+        e0.record()
+        for _ in range(reps):
+            torch.matmul(a, w.t())
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        tf = 2.0 * M * N * K / (us * 1e-6) / 1e12
+        print(json.dumps({"probe": "torch_matmul_f16", "gemm": name, "M": M, "N": N, "K": K,
+                          "us": round(us, 2), "tflops": round(tf, 1),
+                          "frac_of_2500": round(tf / PEAK_F16_TFLOPS, 3)}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -123,6 +168,7 @@ def main() -> int:
     ap.add_argument("--workload", default="xl-720p-stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, metavar="MIB")
+    ap.add_argument("--reference-probes", action="store_true")
     ap.add_argument("--streams", type=int, default=1,
                     help="independent streams decoded concurrently per step (fd_decode_chunks)")
     ap.add_argument("--pixels", choices=["f32", "bf16", "u8"], default="f32",
@@ -135,6 +181,8 @@ def main() -> int:
         return 2
     if args.copy_calibration:
         return copy_calibration(args.copy_calibration)
+    if args.reference_probes:
+        return reference_probes()
 
     import numpy as np
     import torch

@@ -330,6 +330,18 @@ fd_status fd_probe_read(fd_kv_cache* cache, double* total_ms, int64_t* launches,
 fd_status fd_measure_mfma_peak(int32_t dtype, int32_t iters, void* stream, double* tflops,
                                double* clock_ghz);
 
+/* LDS read bandwidth of one compute unit (a measurement aid for the GEMM and
+ * attention kernels, which read their MFMA operands from LDS): two 8-wave
+ * workgroups per compute unit each read 64 KB of LDS with conflict-free
+ * 16-byte loads (8 in flight per wave), `iters` rounds, twice back to back on
+ * `stream` (NULL = default); the second launch's per-workgroup shader cycles
+ * give the bytes per shader clock a compute unit delivers, written with the
+ * mean shader clock (GHz). Blocks until done; allocates and frees its own small
+ * device buffers. iters in [1, 10^7], else INVALID_ARGUMENT; HIP failures give
+ * DEVICE. */
+fd_status fd_measure_lds_bandwidth(int32_t iters, void* stream, double* bytes_per_clock_cu,
+                                   double* clock_ghz);
+
 /* E4M3 quantisation of rows, the rule the FP8 MLP applies to its weights
  * (FD_MLP_PRECISION_FP8): for each row r of in[rows][cols] (row-major fp32),
  * m = max |in[r][:]|, inv = 448 / m (fp32 division), codes[r][c] = the OCP

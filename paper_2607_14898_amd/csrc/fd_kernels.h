@@ -164,6 +164,12 @@ hipError_t swiglu_f32(const float* raw, int M, int H, float* h, hipStream_t stre
 hipError_t mfma_peak(Act16 t, int blocks, int iters, unsigned long long* clk, float* sink,
                      hipStream_t stream);
 
+// LDS read-bandwidth probe: `blocks` workgroups of 8 waves, each wave issuing
+// 8 conflict-free ds_read_b128 per iteration; clk as for mfma_peak, sink
+// blocks * 512 words.
+hipError_t lds_read_probe(int blocks, int iters, unsigned long long* clk, unsigned* sink,
+                          hipStream_t stream);
+
 // Convert a host-prepared fp32 array on the device into 16-bit operands.
 hipError_t convert_f32_to_16(const float* src, void* dst, int64_t n, int out_kind,
                              hipStream_t stream);

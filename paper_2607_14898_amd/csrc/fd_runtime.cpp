@@ -1408,6 +1408,54 @@ fd_status fd_measure_mfma_peak(int32_t dtype, int32_t iters, void* stream, doubl
   return FD_OK;
 }
 
+fd_status fd_measure_lds_bandwidth(int32_t iters, void* stream, double* bytes_per_clock_cu,
+                                   double* clock_ghz) {
+  if (!bytes_per_clock_cu || !clock_ghz) return fail(FD_ERR_INVALID_ARGUMENT, "output pointer is NULL");
+  if (iters < 1 || iters > 10000000) return fail(FD_ERR_INVALID_ARGUMENT, "iters out of range");
+  int dev = 0, cus = 0, wclk_khz = 0;
+  FD_HIP(hipGetDevice(&dev));
+  FD_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  FD_HIP(hipDeviceGetAttribute(&wclk_khz, hipDeviceAttributeWallClockRate, dev));
+  if (cus <= 0 || wclk_khz <= 0) return fail(FD_ERR_DEVICE, "device attributes unavailable");
+  const int per_cu = 2, blocks = per_cu * cus;
+  hipStream_t s = (hipStream_t)stream;
+  unsigned long long* clk = nullptr;
+  unsigned* sink = nullptr;
+  fd_status st = FD_OK;
+  std::vector<unsigned long long> h(2 * (size_t)blocks);
+  do {
+    if (hipMalloc(&clk, h.size() * sizeof(unsigned long long)) != hipSuccess ||
+        hipMalloc(&sink, (size_t)blocks * 512 * sizeof(unsigned)) != hipSuccess) {
+      st = fail(FD_ERR_OUT_OF_MEMORY, "probe buffers");
+      break;
+    }
+    hipError_t e = fd::lds_read_probe(blocks, iters, clk, sink, s);
+    if (e == hipSuccess) e = fd::lds_read_probe(blocks, iters, clk, sink, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e == hipSuccess)
+      e = hipMemcpy(h.data(), clk, h.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) {
+      st = fail(FD_ERR_DEVICE, "LDS probe failed: %s", hipGetErrorString(e));
+      break;
+    }
+  } while (false);
+  if (clk) (void)hipFree(clk);
+  if (sink) (void)hipFree(sink);
+  if (st != FD_OK) return st;
+  // each workgroup: 8 waves x iters x 8 reads x 64 lanes x 16 bytes over its own cycles;
+  // per_cu workgroups share a compute unit
+  const double bytes_wg = 8.0 * iters * 8.0 * 64.0 * 16.0;
+  double rate = 0.0, cyc = 0.0, ticks = 0.0;
+  for (int b = 0; b < blocks; ++b) {
+    rate += bytes_wg / (double)h[2 * b];
+    cyc += (double)h[2 * b];
+    ticks += (double)h[2 * b + 1];
+  }
+  *bytes_per_clock_cu = rate / blocks * per_cu;
+  *clock_ghz = ticks > 0 ? cyc / ticks * wclk_khz * 1e-6 : 0.0;
+  return FD_OK;
+}
+
 fd_status fd_quantize_e4m3_rows(const float* in, int64_t rows, int64_t cols, uint8_t* codes,
                                 float* scales) {
   if (rows < 0 || cols < 1) return fail(FD_ERR_INVALID_ARGUMENT, "rows >= 0 and cols >= 1 required");

@@ -7,7 +7,8 @@
 // two 4-wave workgroups per CU issues 32x32x16 MFMAs back to back on eight
 // accumulators, with operands that change every instruction (pseudo-random
 // values in [-1, 1), like real activations and weights), and records its
-// shader-clock cycles and wall-clock ticks.
+// shader-clock cycles and wall-clock ticks. A second probe measures how many
+// bytes per clock the LDS of a compute unit delivers to ds_read_b128.
 #include "fd_kernels.h"
 
 #include <hip/hip_bf16.h>
@@ -73,7 +74,41 @@ __global__ __launch_bounds__(256) void mfma_peak_kernel(int iters, unsigned long
   }
 }
 
+// LDS read bandwidth: every wave reads 16 bytes per lane per ds_read_b128 from
+// a 64 KB block of LDS, consecutive lanes reading consecutive 16-byte chunks
+// (no bank conflicts), 8 independent reads in flight per step; the values are
+// folded into one register so the reads stay live.
+__global__ __launch_bounds__(512) void lds_read_kernel(int iters, unsigned long long* clk, unsigned* sink) {
+  __shared__ uint4 buf[4096];  // 64 KB
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int i = tid; i < 4096; i += blockDim.x) buf[i] = make_uint4(i, i * 3u, i * 5u, i * 7u);
+  __syncthreads();
+  uint32_t acc = 0;
+  int base = (wave * 512 + lane) & 4095;
+  const unsigned long long c0 = clock64(), w0 = wall_clock64();
+  for (int it = 0; it < iters; ++it) {
+    uint4 v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = buf[(base + 64 * k) & 4095];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc ^= v[k].x ^ v[k].y ^ v[k].z ^ v[k].w;
+    base = (base + 512 + (acc & 1)) & 4095;
+  }
+  const unsigned long long c1 = clock64(), w1 = wall_clock64();
+  sink[blockIdx.x * blockDim.x + tid] = acc;
+  if (tid == 0) {
+    clk[2 * blockIdx.x] = c1 - c0;
+    clk[2 * blockIdx.x + 1] = w1 - w0;
+  }
+}
+
 }  // namespace
+
+hipError_t lds_read_probe(int blocks, int iters, unsigned long long* clk, unsigned* sink, hipStream_t s) {
+  if (blocks <= 0 || iters <= 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(lds_read_kernel, dim3(blocks), dim3(512), 0, s, iters, clk, sink);
+  return hipGetLastError();
+}
 
 hipError_t mfma_peak(Act16 t, int blocks, int iters, unsigned long long* clk, float* sink, hipStream_t s) {
   if (blocks <= 0 || iters <= 0) return hipErrorInvalidValue;

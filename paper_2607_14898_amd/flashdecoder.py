@@ -90,6 +90,8 @@ def load_library() -> ctypes.CDLL:
                                 ctypes.POINTER(ctypes.c_double)]),
         "fd_measure_mfma_peak": (I32, [I32, I32, P, ctypes.POINTER(ctypes.c_double),
                                        ctypes.POINTER(ctypes.c_double)]),
+        "fd_measure_lds_bandwidth": (I32, [I32, P, ctypes.POINTER(ctypes.c_double),
+                                           ctypes.POINTER(ctypes.c_double)]),
         "fd_quantize_e4m3_rows": (I32, [P, I64, I64, P, P]),
         "fd_quantize_e4m3_rows_device": (I32, [P, I64, I64, P, P, P]),
         "fd_pack_e4m3_weight": (I32, [P, I64, I64, P]),
@@ -288,6 +290,15 @@ def fd_probe_read(cache: int):
     ms, n, w = ctypes.c_double(), ctypes.c_int64(), ctypes.c_double()
     _check(load_library().fd_probe_read(cache, ctypes.byref(ms), ctypes.byref(n), ctypes.byref(w)))
     return ms.value, n.value, w.value
+
+
+def fd_measure_lds_bandwidth(iters: int = 20000, stream=None):
+    """(bytes per shader clock per compute unit, shader clock GHz) of conflict-free
+    ds_read_b128 loads on this GPU."""
+    b, g = ctypes.c_double(), ctypes.c_double()
+    _check(load_library().fd_measure_lds_bandwidth(iters, _stream_handle(stream),
+                                                   ctypes.byref(b), ctypes.byref(g)))
+    return b.value, g.value
 
 
 def fd_measure_mfma_peak(dtype: str = "f16", iters: int = 100000, stream=None):

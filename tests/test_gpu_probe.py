@@ -16,3 +16,14 @@ def test_mfma_peak_probe_is_plausible(dtype):
     assert 0.5 < ghz < 2.6
     # cannot exceed one 32x32x16 MFMA per 32 cycles per SIMD at the measured clock
     assert 100.0 < tf <= 2500.0 * ghz / 2.4 * 1.02
+
+
+def test_lds_bandwidth_probe_is_plausible():
+    """Bytes per clock per compute unit of conflict-free ds_read_b128: at least
+    the 64 bytes of one 16-lane group per clock of earlier CDNA parts, at most
+    1 KB, and a shader clock within the chip's range."""
+    from paper_2607_14898_amd import flashdecoder as fdb
+    bpc, ghz = fdb.fd_measure_lds_bandwidth(2000)
+    print(f"LDS read: {bpc:.1f} bytes per clock per CU at {ghz:.2f} GHz", flush=True)
+    assert 32.0 <= bpc <= 1024.0
+    assert 0.5 <= ghz <= 2.6

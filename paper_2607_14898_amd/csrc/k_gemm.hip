@@ -989,6 +989,7 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
 // - Otherwise 128 x 128 tiles with 3 stages, several workgroups per CU, so one
 //   workgroup's epilogue and barriers overlap another's MFMAs.
 using TileL = TileCfg<256, 256, 2, 4, 4>;   // 8 waves of 128 x 64, 128 KB LDS
+using TileW = TileCfg<256, 192, 2, 2, 5>;   // 4 waves of 128 x 96, 140 KB
 using TileM = TileCfg<192, 128, 2, 2, 6>;   // 4 waves of 96 x 64, 120 KB
 using TileS1 = TileCfg<128, 128, 2, 2, 6>;  // 4 waves of 64 x 64, 96 KB
 using TileS = TileCfg<128, 128, 2, 2, 3>;   // 4 waves of 64 x 64, 48 KB
@@ -1002,6 +1003,15 @@ hipError_t dispatch_tiles(const GemmArgs& g, hipStream_t s) {
     // backbone: 336 tiles, 1.3 rounds) runs faster as 128 x 128 tiles, several
     // per CU (measured 1.8% per 480p chunk)
     if (EPI == EPI_SWIGLU && tiles(256, 256) < 512) return launch_gemm<T, TileS, EPI>(g, s);
+    // 256 x 192 tiles where their rounds of 256 CUs, weighted by tile area,
+    // are fewer than those of 256 x 256 tiles (for instance 342 -> 456 tiles,
+    // 2 -> 1.5 round-equivalents, for 14400 x 1536 outputs). Their 96-column
+    // wave blocks suit every epilogue but the paired SwiGLU and the QKV post
+    // step (one 64-column head vector per wave).
+    if constexpr (EPI != EPI_SWIGLU && EPI != EPI_QKV) {
+      const int rounds_l = (tiles(256, 256) + 255) / 256, rounds_w = (tiles(256, 192) + 255) / 256;
+      if (4 * rounds_w * 3 < 4 * rounds_l * 4) return launch_gemm<T, TileW, EPI>(g, s);
+    }
     return launch_gemm<T, TileL, EPI>(g, s);
   }
   const int tm = tiles(192, 128);

@@ -11,6 +11,8 @@ before timing starts. Prints one JSON line.
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
   python bench.py --copy-calibration MIB   (plain device copy of MIB MiB, for
                                             scaling HBM byte counters)
+  python bench.py --cpu-baselines          (the CPU oracle timed in full on the tiny
+                                            workloads and per steady stream call)
   python bench.py --reference-probes       (the GPU's LDS read bandwidth and the
                                             rate of torch.matmul on the decoder's
                                             720p GEMM shapes, as context for the
@@ -41,50 +43,116 @@ ATTN_SOURCE = os.path.join(ROOT, "paper_2607_14898_amd", "csrc", "k_attn.hip")
 METRIC = "decoded frames/sec at 720p (latent->pixel), p50 per-chunk latency, % MFMA peak"
 
 
-def cpu_baseline(wl, weights, gpu_fps_unit_flops):
-    """Time the CPU oracle on a bounded sample of the same workload.
+def _cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
 
-    Sample: backbone blocks 0-3 of chunk 1 (steady state: the window holds
-    chunk 0) of the stream, through oracle.block_forward in fp64. Extrapolated
-    to frames/s with the algorithmic FLOPs of a steady chunk.
-    """
-    import numpy as np
-    import oracle.decoder as od
-    from paper_2607_14898_amd.flops import call_flops
 
-    m = wl.model
+def _blas_threads() -> int:
     try:
         from threadpoolctl import threadpool_info
-        cores = max([d.get("num_threads", 1) for d in threadpool_info()
-                     if d.get("user_api") == "blas"] or [1])
+        return max([d.get("num_threads", 1) for d in threadpool_info() if d.get("user_api") == "blas"] or [1])
     except Exception:
-        cores = os.cpu_count() or 1
-    nblk = 4
-    W = {k: v.astype(np.float64) for k, v in weights.items()
-         if k.startswith("embed.") or any(k.startswith(f"bb.{i}.") for i in range(nblk))}
-    z = wl.latents()[0, :, :2]
-    caches = [[] for _ in range(nblk)]
-    x = []
-    for t in range(2):
-        P = od.pixel_unshuffle_frame(z[:, t].astype(np.float64), m.patch)
-        x.append(P @ W["embed.w"].T + W["embed.b"])
-    for i in range(nblk):    # chunk 0 fills the windows (untimed)
-        x[0] = od.block_forward(m, W, f"bb.{i}", x[0], od.token_positions(m, [0]), 0, caches[i])
+        return os.cpu_count() or 1
+
+
+def time_oracle(wl, weights, n_calls):
+    """Wall time of the CPU oracle (fp32, numpy with the host's BLAS threads)
+    decoding the first n_calls calls of workload wl, and the frames it emits."""
+    import numpy as np
+    from oracle.decoder import StreamingOracle
+    m = wl.model
+    z = wl.latents()
+    F = wl.frames_per_call
     t0 = time.perf_counter()
-    for i in range(nblk):
-        x[1] = od.block_forward(m, W, f"bb.{i}", x[1], od.token_positions(m, [1]), 1, caches[i])
+    for b in range(z.shape[0]):
+        dec = StreamingOracle(m, weights, np.float32)
+        for c in range(n_calls):
+            dec.decode(z[b, :, c * F:(c + 1) * F])
     dt = time.perf_counter() - t0
-    L, D, G, Dh = m.tokens_per_frame, m.dim, m.n_kv_groups, m.head_dim
-    block_flops = nblk * (2.0 * L * (D * (D + 2 * G * Dh) + D * D + 3 * D * m.mlp_hidden) +
-                          4.0 * m.n_heads * L * (2 * L) * Dh)
-    chunk_flops = sum(call_flops(m, wl.frames_per_call, 5))
-    chunk_s = dt * chunk_flops / block_flops
-    fps = wl.frames_per_call * m.r_t / chunk_s
-    return {"value": round(fps, 5), "unit": "frames/s", "cores": int(cores), "kind": "oracle",
-            "sample": (f"backbone blocks 0-{nblk - 1} of chunk 1 of the {wl.name} stream (fp64 numpy oracle, "
-                       f"{block_flops / 1e12:.3f} TFLOP in {dt:.2f} s), extrapolated by "
-                       f"algorithmic FLOPs to a steady chunk ({chunk_flops / 1e12:.2f} TFLOP)"),
-            "cpu": platform.processor() or platform.machine()}
+    return dt, z.shape[0] * n_calls * F * m.r_t
+
+
+def time_oracle_steady_chunk(wl, weights, rf_frac=5):
+    """CPU seconds of one steady call (one latent frame, the window full) of a
+    one-frame-per-call stream, from the fp32 oracle timed on parts of it:
+    backbone block 0 in full (all queries against the two visible frames'
+    keys) counted once per backbone block; refinement block 0 for 1/rf_frac
+    of the call's queries (against all visible keys) counted rf_frac times per
+    refinement block; the latent projection, temporal upsampling and pixel
+    head in full. Returns (seconds, measured seconds, description)."""
+    import numpy as np
+    import oracle.decoder as od
+    m = wl.model
+    L, r = m.tokens_per_frame, m.r_t
+    W = {k: np.asarray(v, np.float32) for k, v in weights.items()
+         if k.startswith(("embed.", "bb.0.", "rf.0.", "bb.norm_f", "rf.norm_f", "tup.", "head"))}
+    z = wl.latents()[0, :, :2].astype(np.float32)
+    meas = 0.0
+    t = time.perf_counter()
+    x = [od.pixel_unshuffle_frame(z[:, c], m.patch) @ W["embed.w"].T + W["embed.b"] for c in (0, 1)]
+    t_embed = (time.perf_counter() - t) / 2
+    pos_k = np.concatenate([od.token_positions(m, [c]) for c in (0, 1)])
+    t = time.perf_counter()
+    y_bb = od.block_forward_rows(m, W, "bb.0", np.concatenate(x), pos_k, x[1], od.token_positions(m, [1]))
+    t_bb = time.perf_counter() - t
+    # refinement inputs: the temporal upsampling of both frames' (block-0) states
+    t = time.perf_counter()
+    xr = [od.temporal_up_rows(m, W, od.stack_final(m, W, "bb", xc)).transpose(1, 0, 2).reshape(r * L, m.dim)
+          for xc in (x[0], y_bb)]
+    t_tup = (time.perf_counter() - t) / 2
+    rows = np.arange(0, r * L, rf_frac)
+    rpos_k = np.concatenate([od.token_positions(m, [r * c + j for j in range(r)]) for c in (0, 1)])
+    rpos_q = od.token_positions(m, [r + j for j in range(r)])[rows]
+    t = time.perf_counter()
+    y_rf = od.block_forward_rows(m, W, "rf.0", np.concatenate(xr), rpos_k, xr[1][rows], rpos_q)
+    t_rf = time.perf_counter() - t
+    t = time.perf_counter()
+    od.head_rows(m, W, od.stack_final(m, W, "rf", y_rf))
+    t_head = time.perf_counter() - t
+    meas = 2 * t_embed + t_bb + 2 * t_tup + t_rf + t_head
+    total = (t_embed + m.n_backbone_blocks * t_bb + t_tup +
+             rf_frac * (m.n_refine_blocks * t_rf + t_head))
+    desc = (f"one steady call of the {wl.name} stream from the fp32 numpy oracle timed on its parts: "
+            f"backbone block 0 in full ({t_bb:.2f} s) x {m.n_backbone_blocks} blocks, refinement block 0 on "
+            f"1/{rf_frac} of the {r * L} queries against all {2 * r * L} keys ({t_rf:.2f} s) x {rf_frac} x "
+            f"{m.n_refine_blocks} blocks, pixel head on the same rows ({t_head:.2f} s) x {rf_frac}, latent "
+            f"projection and temporal upsampling in full; {meas:.1f} s measured")
+    return total, meas, desc
+
+
+def cpu_baseline(wl, weights):
+    """The CPU oracle on a bounded sample of the same workload (one steady
+    call, timed on parts of it), scaled to frames per second."""
+    sec, _, desc = time_oracle_steady_chunk(wl, weights)
+    frames = wl.frames_per_call * wl.model.r_t
+    return {"value": round(frames / sec, 5), "unit": "frames/s", "cores": int(_blas_threads()),
+            "kind": "oracle", "sample": desc, "cpu": _cpu_model()}
+
+
+def cpu_baselines() -> int:
+    """The oracle (fp32) timed in full on the tiny workloads, and per steady
+    call of the streams from timed parts (one JSON line each)."""
+    from paper_2607_14898_amd.workloads import WORKLOADS
+    for name in ("tiny", "tiny-asis"):
+        wl = WORKLOADS[name]
+        dt, frames = time_oracle(wl, wl.weights(), wl.n_calls)
+        print(json.dumps({"workload": name, "calls": wl.n_calls, "frames": frames, "seconds": round(dt, 3),
+                          "frames_per_s": round(frames / dt, 3), "timed": "in full", "dtype": "f32",
+                          "blas_threads": _blas_threads(), "cpu": _cpu_model()}), flush=True)
+    for name in ("xl-480p-stream", "xl-720p-stream"):
+        wl = WORKLOADS[name]
+        sec, meas, desc = time_oracle_steady_chunk(wl, wl.weights())
+        frames = wl.frames_per_call * wl.model.r_t
+        print(json.dumps({"workload": name, "seconds_per_call": round(sec, 1),
+                          "frames_per_s": round(frames / sec, 5), "timed": desc, "dtype": "f32",
+                          "blas_threads": _blas_threads(), "cpu": _cpu_model()}), flush=True)
+    return 0
 
 
 def counter_traffic():
@@ -169,6 +237,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, metavar="MIB")
     ap.add_argument("--reference-probes", action="store_true")
+    ap.add_argument("--cpu-baselines", action="store_true",
+                    help="time the CPU oracle on the tiny workloads and per steady stream call")
     ap.add_argument("--streams", type=int, default=1,
                     help="independent streams decoded concurrently per step (fd_decode_chunks)")
     ap.add_argument("--pixels", choices=["f32", "bf16", "u8"], default="f32",
@@ -183,6 +253,8 @@ def main() -> int:
         return copy_calibration(args.copy_calibration)
     if args.reference_probes:
         return reference_probes()
+    if args.cpu_baselines:
+        return cpu_baselines()
 
     import numpy as np
     import torch
@@ -313,7 +385,7 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f16+fp8" if fp8 else "f16",
+        "dtype": (m.compute_dtype + "+fp8") if fp8 else m.compute_dtype,
         "data": "synthetic",
         "config": {
             "workload": wl.name,
@@ -332,7 +404,7 @@ def main() -> int:
             "mfma_frac_overall": round(flops / wall / 1e12 / PEAK_F16_TFLOPS, 4),
             "mfma_frac_overall_of_measured_peak": round(flops / wall / 1e12 / peak_meas, 4),
             "algorithmic_tflop_per_step": round(flops / K / 1e12, 4),
-            "operands": "fp16 MFMA operands (bf16-rounded weights/latents), fp32 accumulate",
+            "operands": f"{m.compute_dtype} MFMA operands (bf16-rounded weights/latents), fp32 accumulate",
             "paper_context": "76.1 frames/s, FlashDecoder-XL Wan2.1 720p streaming, 1x H100 (Table 2)",
         },
         "kernel_classes": kclasses,
@@ -354,7 +426,7 @@ def main() -> int:
         },
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(wl, weights, None)
+        result["cpu_baseline"] = cpu_baseline(wl, weights)
     print(json.dumps(result), flush=True)
     for c in caches:
         c.close()

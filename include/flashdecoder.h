@@ -175,6 +175,17 @@ fd_status fd_kv_cache_reset(fd_kv_cache* cache);
 /* Latent frames decoded since the last reset, or -1 for NULL. */
 int64_t fd_kv_cache_position(const fd_kv_cache* cache);
 
+/* fp16 range guard of the 16-bit path with fp16 operands: hidden
+ * activations that enter the next GEMM as fp16 (the SwiGLU output of every
+ * block and the pixel head's SiLU output) are clamped to +-65504 instead of
+ * overflowing to infinity, and the clamped values are counted per cache. The
+ * other fp16 operands are bounded by construction (normalised rows, KV-normed
+ * keys and values, convex combinations of those values). Writes the number of
+ * values clamped since the cache's creation or the previous call and clears
+ * it; 0 for the bf16 and fp32 paths. Synchronises the device first. Host
+ * pointer `count`; NULL arguments give INVALID_ARGUMENT. */
+fd_status fd_kv_cache_fp16_saturations(fd_kv_cache* cache, uint64_t* count);
+
 /* Free a cache (NULL is ignored). No work using it may be in flight. */
 void fd_kv_cache_destroy(fd_kv_cache* cache);
 

@@ -73,6 +73,9 @@ struct EpiParams {
   int row_scale_stride = 1;          // 0: one scale for every row (static per-tensor)
   const float* out_scale = nullptr;  // EPI_SWIGLU_E4M3: {scale, inverse scale} of the codes
   QkvPostArgs qkv;          // EPI_QKV geometry and destinations (raw unused)
+  // fp16 SwiGLU / SiLU outputs beyond +-65504 are clamped to it; when set,
+  // the number of clamped values is added here
+  unsigned* sat = nullptr;
 };
 
 struct GemmArgs {

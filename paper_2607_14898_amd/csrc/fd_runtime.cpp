@@ -313,6 +313,7 @@ struct fd_kv_cache {
   int U_bb = 0, U_bb_pad = 0, U_rf = 0, U_rf_pad = 0;
   void* ring = nullptr;
   std::vector<void*> k_bb, v_bb, k_rf, v_rf;
+  unsigned* sat = nullptr;  // fp16 hidden values clamped to +-65504 (zeroed with the ring)
   void* ws = nullptr;
   float *x_bb = nullptr, *x_rf = nullptr, *raw = nullptr;
   void *a = nullptr, *q = nullptr, *o = nullptr, *h = nullptr, *u = nullptr;
@@ -531,6 +532,7 @@ fd_status run_stack(Ctx& x, const std::vector<LayerW>& layers, float* xs, int ro
       const float* sc = dec->act_sc + 4 * (layer0 + (int)l);
       if ((st = run_norm(x, xs, rows, w.n2g, w.n2b, true, sc))) return st;
       g = gemm_args(kc->a8, D, w.w1, rows, 2 * H, D, fd::EPI_SWIGLU_E4M3, w.b1);
+      g.ep.sat = kc->sat;
       g.ep.out_a = kc->h8;
       g.ep.ld_out = H;
       g.ep.row_scale = sc;
@@ -555,6 +557,7 @@ fd_status run_stack(Ctx& x, const std::vector<LayerW>& layers, float* xs, int ro
       unsigned* cal = x.calibrate ? dec->calib + 2 * (layer0 + (int)l) : nullptr;
       if ((st = run_norm(x, xs, rows, w.n2g, w.n2b, true, nullptr, cal))) return st;
       g = gemm_args(kc->a8, D, w.w1, rows, 2 * H, D, fd::EPI_SWIGLU, w.b1);
+      g.ep.sat = kc->sat;
       g.ep.out_a = kc->h;
       g.ep.ld_out = H;
       g.ep.row_scale = kc->sa;
@@ -577,6 +580,7 @@ fd_status run_stack(Ctx& x, const std::vector<LayerW>& layers, float* xs, int ro
     if (c.mlp_kind == FD_MLP_SWIGLU) {
       if (d.is16) {
         g = gemm_args(kc->a, D, w.w1, rows, 2 * H, D, fd::EPI_SWIGLU, w.b1);
+        g.ep.sat = kc->sat;
         g.ep.out_a = kc->h;
         g.ep.ld_out = H;
         if ((st = run_gemm(x, g, D))) return st;
@@ -671,6 +675,7 @@ fd_status decode(const fd_decoder* dec, const void* latent, int32_t latent_dtype
                           kc->U_rf_pad, kc->t * c.r_t, kc->k_rf, kc->v_rf, true))) break;
       if ((st = run_norm(x, kc->x_rf, MR, dec->rff_g, dec->rff_b))) break;
       g = gemm_args(kc->a, D, dec->head1_w, MR, c.head_hidden, D, fd::EPI_STORE_SILU, dec->head1_b);
+      g.ep.sat = kc->sat;
       g.ep.out_a = kc->h;
       g.ep.ld_out = c.head_hidden;
       if ((st = run_gemm(x, g, D))) break;
@@ -1140,8 +1145,8 @@ fd_status fd_kv_cache_create(const fd_decoder* dec, int32_t batch, fd_kv_cache**
   const size_t ring_bb = (size_t)batch * G * kc->S * kc->U_bb_pad * Dh * es;
   const size_t ring_rf = (size_t)batch * G * kc->S * kc->U_rf_pad * Dh * es;
   const int nb = c.n_backbone_blocks, nr = tf ? c.n_refine_blocks : 0;
-  const size_t ring_total = 2 * (nb * ring_bb + nr * ring_rf);
-  if (ring_total) {
+  const size_t ring_total = 2 * (nb * ring_bb + nr * ring_rf) + 256;  // + the saturation counter
+  {
     if (hipMalloc(&kc->ring, ring_total) != hipSuccess) {
       free_cache(kc);
       return fail(FD_ERR_OUT_OF_MEMORY, "KV ring: hipMalloc(%zu) failed", ring_total);
@@ -1160,6 +1165,7 @@ fd_status fd_kv_cache_create(const fd_decoder* dec, int32_t batch, fd_kv_cache**
     kc->k_rf.push_back(p); p += ring_rf;
     kc->v_rf.push_back(p); p += ring_rf;
   }
+  kc->sat = (unsigned*)p;
   // workspace for the largest call
   const WsLayout w = ws_layout(c, d, (int64_t)batch * c.max_frames_per_call * d.L);
   if (hipMalloc(&kc->ws, w.total) != hipSuccess) {
@@ -1178,6 +1184,24 @@ fd_status fd_kv_cache_reset(fd_kv_cache* cache) {
 }
 
 int64_t fd_kv_cache_position(const fd_kv_cache* cache) { return cache ? cache->t : -1; }
+
+fd_status fd_kv_cache_fp16_saturations(fd_kv_cache* cache, uint64_t* count) {
+  if (!cache || !count) return fail(FD_ERR_INVALID_ARGUMENT, "NULL argument");
+  *count = 0;
+  int prev = 0;
+  FD_HIP(hipGetDevice(&prev));
+  const int dev = cache->dec->device;
+  if (prev != dev) FD_HIP(hipSetDevice(dev));
+  unsigned v = 0;
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess) e = hipMemcpy(&v, cache->sat, sizeof v, hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemset(cache->sat, 0, sizeof v);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (prev != dev) (void)hipSetDevice(prev);
+  if (e != hipSuccess) return fail(FD_ERR_DEVICE, "reading the saturation counter failed: %s", hipGetErrorString(e));
+  *count = v;
+  return FD_OK;
+}
 
 void fd_kv_cache_destroy(fd_kv_cache* cache) { free_cache(cache); }
 

@@ -19,6 +19,8 @@
 #include <hip/hip_bf16.h>
 #include <hip/hip_fp16.h>
 
+#include <type_traits>
+
 namespace fd {
 namespace {
 
@@ -38,6 +40,28 @@ template <> __device__ __forceinline__ __hip_bfloat16 to_act<__hip_bfloat16>(flo
 __device__ __forceinline__ uint32_t bits16(_Float16 x) { return __builtin_bit_cast(uint16_t, x); }
 __device__ __forceinline__ uint32_t bits16(__hip_bfloat16 x) { return __bfloat16_as_ushort(x); }
 template <> __device__ __forceinline__ float to_act<float>(float v) { return v; }
+
+// A value bound for a 16-bit operand, clamped to the fp16 range when T is
+// fp16 (+-65504; NaN passes unchanged), counting the clamped values in n.
+template <typename T>
+__device__ __forceinline__ float sat16(float v, int& n) {
+  if constexpr (std::is_same<T, _Float16>::value) {
+    const bool big = fabsf(v) > 65504.f;
+    n += big;
+    return big ? copysignf(65504.f, v) : v;
+  } else {
+    return v;
+  }
+}
+
+// Adds this wave's count of clamped values to *sat (one atomic per wave that
+// clamped anything).
+__device__ __forceinline__ void count_sat(unsigned* sat, int n) {
+  if (!sat || __builtin_amdgcn_ballot_w64(n != 0) == 0) return;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) n += __shfl_xor(n, o);
+  if ((threadIdx.x & 63) == 0) atomicAdd(sat, (unsigned)n);
+}
 
 // Every epilogue stores to out[row_off(row) + col_off(col)]: the destination
 // offset splits into a part that depends only on the output row and a part
@@ -443,6 +467,7 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
   // column's then its row's dequantisation scale right before use
   static_assert(!SCALED || EPI == EPI_SWIGLU || EPI == EPI_SWIGLU_E4M3, "scaled transposed epilogue: SwiGLU only");
   typedef __attribute__((ext_vector_type(4))) float f4;
+  int nsat = 0;  // fp16 values clamped to +-65504 by this lane
   int64_t ro[FM];
   bool rok[FM];
 #pragma unroll
@@ -485,7 +510,7 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
               g = g * sg[e] * rs[i];
               u = u * su[e] * rs[i];
             }
-            o4[e] = to_act<T>(silu_f(g + bg[e]) * (u + bu[e]));
+            o4[e] = to_act<T>(sat16<T>(silu_f(g + bg[e]) * (u + bu[e]), nsat));
             h4[e] = (float)o4[e];
           }
           if constexpr (EPI == EPI_SWIGLU_E4M3) {
@@ -521,7 +546,10 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               const int n = c0 + j * 32 + 8 * q + 4 * lk + e;
-              if (rok[i] && n < N)
+              if (!(rok[i] && n < N)) continue;
+              if constexpr (EPI == EPI_STORE_SILU)
+                ((T*)ep.out_a)[ro[i] + col_off<EPI>(ep, n)] = to_act<T>(sat16<T>(silu_f(acc[i][j][4 * q + e] + cb[q][e]), nsat));
+              else
                 epi_store<EPI, T, PXF>(ep, ro[i] + col_off<EPI>(ep, n), acc[i][j][4 * q + e] + cb[q][e]);
             }
         continue;
@@ -563,7 +591,7 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
               T o4[4];
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
-                if constexpr (EPI == EPI_STORE_SILU) o4[e] = to_act<T>(silu_f(v[e]));
+                if constexpr (EPI == EPI_STORE_SILU) o4[e] = to_act<T>(sat16<T>(silu_f(v[e]), nsat));
                 else if constexpr (EPI == EPI_STORE_GELU) o4[e] = to_act<T>(gelu_f(v[e]));
                 else o4[e] = to_act<T>(v[e]);
               }
@@ -573,6 +601,7 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
       }
     }
   }
+  if constexpr (EPI == EPI_SWIGLU || EPI == EPI_SWIGLU_E4M3 || EPI == EPI_STORE_SILU) count_sat(ep.sat, nsat);
 }
 
 // ---------------------------------------------------------------------------

@@ -76,6 +76,7 @@ def load_library() -> ctypes.CDLL:
         "fd_kv_cache_create": (I32, [P, I32, ctypes.POINTER(P)]),
         "fd_kv_cache_reset": (I32, [P]),
         "fd_kv_cache_position": (I64, [P]),
+        "fd_kv_cache_fp16_saturations": (I32, [P, ctypes.POINTER(ctypes.c_uint64)]),
         "fd_kv_cache_destroy": (None, [P]),
         "fd_output_shape": (I32, [P, I32, I32, ctypes.POINTER(I64)]),
         "fd_decode_chunk": (I32, [P, P, I32, I32, P, P, P]),
@@ -408,6 +409,12 @@ class KvCache:
 
     def reset(self) -> None:
         fd_kv_cache_reset(self.handle)
+
+    def fp16_saturations(self) -> int:
+        """fp16 hidden values clamped to +-65504 since the last read (then cleared)."""
+        n = ctypes.c_uint64()
+        _check(load_library().fd_kv_cache_fp16_saturations(self.handle, ctypes.byref(n)))
+        return n.value
 
     @property
     def position(self) -> int:

@@ -290,6 +290,10 @@ WORKLOADS = {
                                    weight_seed=0, latent_seed=103),
     "xl-720p-chunk-fp8": Workload("xl-720p-chunk-fp8", replace(XL_720P, mlp_precision="fp8"), 4, 1,
                                   weight_seed=0, latent_seed=104),
+    # the same 720p stream with bf16 MFMA operands (the operand type of the
+    # paper's bf16 training) instead of fp16
+    "xl-720p-stream-bf16": Workload("xl-720p-stream-bf16", replace(XL_720P, compute_dtype="bf16"), 1, 32,
+                                    weight_seed=0, latent_seed=105),
     # 1080p stream (Table 2's third resolution): padded latent row, output cropped to 1080 rows
     "xl-1080p-stream": Workload("xl-1080p-stream", XL_1080P, 1, 8, weight_seed=0, latent_seed=108,
                                 pad_rows=1),

@@ -316,3 +316,30 @@ def test_f16_all_negative_logits_match_oracle():
     rel = np.abs(got - ref).max() / np.sqrt(np.mean(ref ** 2))
     print(f"largest logit {log2_max:.1f} (log2 units); relative max error {rel:.3e}", flush=True)
     assert rel <= TOL_16
+
+
+def test_f16_hidden_beyond_fp16_range_is_clamped_and_counted():
+    """A SwiGLU projection scaled by 256 (exact in bf16 and fp16) drives hidden
+    values past 65504: they are clamped to the fp16 range and counted, and the
+    pixels stay finite; the unscaled decoder clamps nothing."""
+    import torch
+    from paper_2607_14898_amd import flashdecoder as fdb
+    m = XL_NARROW
+    W = make_weights(m, 0)
+    z = torch.from_numpy(make_latents(m, 2, 43)).cuda()
+    counts = []
+    for scale in (1.0, 256.0):
+        Ws = dict(W)
+        Ws["bb.0.w13"] = W["bb.0.w13"] * np.float32(scale)
+        dec = fdb.Decoder(m, Ws, max_batch=1, max_frames_per_call=1)
+        cache = fdb.KvCache(dec, 1)
+        outs = [cache.decode_chunk(z[:, :, t:t + 1].contiguous()) for t in range(2)]
+        torch.cuda.synchronize()
+        counts.append(cache.fp16_saturations())
+        assert cache.fp16_saturations() == 0          # the read cleared it
+        assert all(torch.isfinite(o).all().item() for o in outs)
+        cache.close()
+        dec.close()
+    print(f"clamped hidden values: unscaled {counts[0]}, scaled {counts[1]}", flush=True)
+    assert counts[0] == 0 and counts[1] > 0
+

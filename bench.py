@@ -13,6 +13,8 @@ before timing starts. Prints one JSON line.
                                             scaling HBM byte counters)
   python bench.py --cpu-baselines          (the CPU oracle timed in full on the tiny
                                             workloads and per steady stream call)
+  python bench.py --trace-gaps CSV         (idle time between a call's kernels in a
+                                            rocprofv3 kernel trace of this script)
   python bench.py --reference-probes       (the GPU's LDS read bandwidth and the
                                             rate of torch.matmul on the decoder's
                                             720p GEMM shapes, as context for the
@@ -155,6 +157,44 @@ def cpu_baselines() -> int:
     return 0
 
 
+def trace_gaps(path: str, warmup: int, steps: int) -> int:
+    """Idle time between the kernels of each timed decode call in a rocprofv3
+    kernel trace (--kernel-trace --output-format csv) of this script run with
+    the same --warmup and --steps: per call, from the latent unshuffle to the
+    pixel-store GEMM, the wall span against the union of kernel intervals.
+    Host-only; prints one JSON line."""
+    import csv
+    import numpy as np
+    ks = sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"])
+                for r in csv.DictReader(open(path)))
+    starts = [i for i, k in enumerate(ks) if "unshuffle_kernel" in k[2]]
+    calls = []
+    for a, b in zip(starts, starts[1:] + [len(ks)]):
+        seg = ks[a:b]
+        ends = [i for i, k in enumerate(seg) if "Li7EEEv" in k[2]]  # the EPI_PIXEL GEMM
+        if not ends:
+            continue
+        seg = seg[:ends[-1] + 1]
+        busy, cs, ce = 0, None, None
+        for s0, e0, _ in seg:
+            if ce is None or s0 > ce:
+                if ce is not None:
+                    busy += ce - cs
+                cs, ce = s0, e0
+            else:
+                ce = max(ce, e0)
+        busy += ce - cs
+        gaps = [seg[i + 1][0] - seg[i][1] for i in range(len(seg) - 1)]
+        calls.append((seg[-1][1] - seg[0][0], busy, len(seg), float(np.median(gaps)), max(gaps)))
+    c = np.array(calls[warmup:warmup + steps])   # the timed calls follow the warmup ones
+    span, busy = c[:, 0].mean() / 1e3, c[:, 1].mean() / 1e3
+    print(json.dumps({"calls": len(c), "kernels_per_call": round(float(c[:, 2].mean()), 1),
+                      "span_us": round(span, 1), "busy_us": round(busy, 1), "idle_us": round(span - busy, 1),
+                      "idle_frac": round((span - busy) / span, 5), "median_gap_us": round(float(np.median(c[:, 3])) / 1e3, 2),
+                      "max_gap_us": round(float(c[:, 4].max()) / 1e3, 1)}), flush=True)
+    return 0
+
+
 def counter_traffic():
     """HBM bytes per launch of the refinement attention from the committed
     counter summary, or None if it is missing or was taken on other source."""
@@ -237,6 +277,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, metavar="MIB")
     ap.add_argument("--reference-probes", action="store_true")
+    ap.add_argument("--trace-gaps", metavar="CSV",
+                    help="idle time between a decode call's kernels in a rocprofv3 kernel trace (host only)")
     ap.add_argument("--cpu-baselines", action="store_true",
                     help="time the CPU oracle on the tiny workloads and per steady stream call")
     ap.add_argument("--streams", type=int, default=1,
@@ -253,6 +295,8 @@ def main() -> int:
         return copy_calibration(args.copy_calibration)
     if args.reference_probes:
         return reference_probes()
+    if args.trace_gaps:
+        return trace_gaps(args.trace_gaps, args.warmup, args.steps)
     if args.cpu_baselines:
         return cpu_baselines()
 

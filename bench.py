@@ -238,7 +238,8 @@ GEMM_SHAPES_720P = [
 
 
 def reference_probes() -> int:
-    """LDS bandwidth of a compute unit (fd_measure_lds_bandwidth), and torch.matmul
+    """LDS bandwidth of a compute unit (fd_measure_lds_bandwidth), the overlap of
+    MFMAs and vector instructions (fd_measure_issue_overlap), and torch.matmul
     (the vendor BLAS) on the decoder's GEMM shapes with random fp16 operands: a
     reference point for the library's own GEMM kernels, never used by them."""
     import torch
@@ -246,6 +247,10 @@ def reference_probes() -> int:
     bpc, ghz = fdb.fd_measure_lds_bandwidth(20000)
     print(json.dumps({"probe": "lds_read_bandwidth", "bytes_per_clock_per_cu": round(bpc, 1),
                       "clock_ghz": round(ghz, 3)}), flush=True)
+    for wps in (1, 2):
+        cyc = fdb.fd_measure_issue_overlap(wps, 20000)
+        print(json.dumps({"probe": "issue_overlap", "waves_per_simd": wps,
+                          "cycles_per_slot": {k: round(v, 1) for k, v in cyc.items()}}), flush=True)
     torch.manual_seed(0)
     for name, M, N, K in GEMM_SHAPES_720P:
         a = (torch.randn(M, K, device="cuda") * 0.5).half()

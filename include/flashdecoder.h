@@ -353,6 +353,19 @@ fd_status fd_measure_mfma_peak(int32_t dtype, int32_t iters, void* stream, doubl
 fd_status fd_measure_lds_bandwidth(int32_t iters, void* stream, double* bytes_per_clock_cu,
                                    double* clock_ghz);
 
+/* How far a wave's MFMAs and its vector instructions overlap (a measurement
+ * aid for the attention kernel, whose exponentials share the SIMD with its
+ * MFMAs): on every compute unit one workgroup with waves_per_simd (1 or 2)
+ * waves per SIMD, `iters` iterations of 4 slots on `stream` (NULL = default). A slot is,
+ * by mode: 0 one 32x32x16 f16 MFMA; 1 four exponentials (each with a
+ * multiply); 2 both; 3 eight fused multiply-adds; 4 MFMA and eight FMAs; 5
+ * MFMA, four exponentials and four FMAs; every slot's instructions are
+ * independent of the other slots'. cycles[0..5] receive the mean shader cycles
+ * per slot and wave. Blocks until done; allocates and frees its own small
+ * device buffers. waves_per_simd outside {1, 2} or iters outside [1, 10^7]
+ * give INVALID_ARGUMENT; HIP failures give DEVICE. */
+fd_status fd_measure_issue_overlap(int32_t waves_per_simd, int32_t iters, void* stream, double* cycles);
+
 /* E4M3 quantisation of rows, the rule the FP8 MLP applies to its weights
  * (FD_MLP_PRECISION_FP8): for each row r of in[rows][cols] (row-major fp32),
  * m = max |in[r][:]|, inv = 448 / m (fp32 division), codes[r][c] = the OCP

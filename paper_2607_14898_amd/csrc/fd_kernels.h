@@ -173,6 +173,14 @@ hipError_t mfma_peak(Act16 t, int blocks, int iters, unsigned long long* clk, fl
 hipError_t lds_read_probe(int blocks, int iters, unsigned long long* clk, unsigned* sink,
                           hipStream_t stream);
 
+// MFMA / vector-instruction issue overlap probe: `blocks` workgroups of
+// 4 waves_per_simd waves (1 or 2 per SIMD) run mode 0..5 (MFMA only; 4
+// exponentials; MFMA + 4 exponentials; 8 FMAs; MFMA + 8 FMAs; MFMA + 4
+// exponentials + 4 FMAs per slot, 4 slots per iteration); clk receives each
+// workgroup's shader cycles, sink blocks * 256 * waves_per_simd floats.
+hipError_t issue_overlap_probe(int mode, int blocks, int waves_per_simd, int iters, unsigned long long* clk,
+                               float* sink, hipStream_t stream);
+
 // Convert a host-prepared fp32 array on the device into 16-bit operands.
 hipError_t convert_f32_to_16(const float* src, void* dst, int64_t n, int out_kind,
                              hipStream_t stream);

@@ -1432,6 +1432,45 @@ fd_status fd_measure_mfma_peak(int32_t dtype, int32_t iters, void* stream, doubl
   return FD_OK;
 }
 
+fd_status fd_measure_issue_overlap(int32_t waves_per_simd, int32_t iters, void* stream, double* cycles) {
+  if (!cycles) return fail(FD_ERR_INVALID_ARGUMENT, "output pointer is NULL");
+  if (iters < 1 || iters > 10000000) return fail(FD_ERR_INVALID_ARGUMENT, "iters out of range");
+  if (waves_per_simd < 1 || waves_per_simd > 2) return fail(FD_ERR_INVALID_ARGUMENT, "waves_per_simd must be 1 or 2");
+  int dev = 0, cus = 0;
+  FD_HIP(hipGetDevice(&dev));
+  FD_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  if (cus <= 0) return fail(FD_ERR_DEVICE, "device attributes unavailable");
+  const int blocks = cus;  // one workgroup of 4 waves_per_simd waves per compute unit
+  hipStream_t s = (hipStream_t)stream;
+  unsigned long long* clk = nullptr;
+  float* sink = nullptr;
+  fd_status st = FD_OK;
+  std::vector<unsigned long long> h((size_t)blocks);
+  do {
+    if (hipMalloc(&clk, h.size() * sizeof(unsigned long long)) != hipSuccess ||
+        hipMalloc(&sink, (size_t)blocks * 256 * waves_per_simd * sizeof(float)) != hipSuccess) {
+      st = fail(FD_ERR_OUT_OF_MEMORY, "probe buffers");
+      break;
+    }
+    for (int mode = 0; mode < 6 && st == FD_OK; ++mode) {
+      hipError_t e = fd::issue_overlap_probe(mode, blocks, waves_per_simd, iters, clk, sink, s);
+      if (e == hipSuccess) e = hipStreamSynchronize(s);
+      if (e == hipSuccess)
+        e = hipMemcpy(h.data(), clk, h.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost);
+      if (e != hipSuccess) {
+        st = fail(FD_ERR_DEVICE, "overlap probe failed: %s", hipGetErrorString(e));
+        break;
+      }
+      double sum = 0.0;
+      for (int b = 0; b < blocks; ++b) sum += (double)h[b];
+      cycles[mode] = sum / blocks / iters / 4.0;  // shader cycles per slot
+    }
+  } while (false);
+  if (clk) (void)hipFree(clk);
+  if (sink) (void)hipFree(sink);
+  return st;
+}
+
 fd_status fd_measure_lds_bandwidth(int32_t iters, void* stream, double* bytes_per_clock_cu,
                                    double* clock_ghz) {
   if (!bytes_per_clock_cu || !clock_ghz) return fail(FD_ERR_INVALID_ARGUMENT, "output pointer is NULL");

@@ -616,9 +616,12 @@ constexpr int BKD = 32;  // K-columns per stage: 4 chunks of 16 bytes per row
 
 // Tile configuration: BM x BN output tile, WAVES_M x WAVES_N wave64s (each a
 // (BM / WAVES_M) x (BN / WAVES_N) sub-tile of 32 x 32 MFMA blocks), NS stages.
-template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int NS_>
+template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int NS_, bool IL_ = false>
 struct TileCfg {
   static constexpr int BM = BM_, BN = BN_, WAVES_M = WAVES_M_, WAVES_N = WAVES_N_, NS = NS_;
+  // IL: the stage refill DMAs are spread between the MFMAs instead of issued
+  // as one burst between two k-steps
+  static constexpr bool IL = IL_;
   static constexpr int NW = WAVES_M * WAVES_N, NT = 64 * NW;
   static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N, FM = WM / 32, FN = WN / 32;
   static constexpr int STAGE = (BM + BN) * 4;                 // 16-byte slots per stage
@@ -689,22 +692,23 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
                      : (uint32_t)(q - BM / 16) * KB * 1024u + (uint32_t)(lrow * 64 + lchunk * 16);
   }
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint4*)lds;
-  auto dma = [&](int st, int kt) {
-    const uint32_t soffA = (uint32_t)kt * BKD * (uint32_t)sizeof(T), soffB = (uint32_t)kt * 1024u;
-#pragma unroll
-    for (int j = 0; j < Q; ++j) {
-      const uint32_t soff = j < QA ? soffA : soffB;
-      const uint32_t m0addr = lds0 + (uint32_t)(st * STAGE + 64 * (j * NW + wave)) * 16u;
-      // M0 is reserved by the compiler, but nothing else in this kernel reads it
-      // (no LDS DMA builtins, interpolation, GWS or message sends).
+  // DMA instruction j of the refill of stage st with K tile kt
+  auto dma1 = [&](int st, int kt, int j) {
+    const uint32_t soff = j < QA ? (uint32_t)kt * BKD * (uint32_t)sizeof(T) : (uint32_t)kt * 1024u;
+    const uint32_t m0addr = lds0 + (uint32_t)(st * STAGE + 64 * (j * NW + wave)) * 16u;
+    // M0 is reserved by the compiler, but nothing else in this kernel reads it
+    // (no LDS DMA builtins, interpolation, GWS or message sends).
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
-      asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-                   :
-                   : "s"(m0addr), "v"(voff[j]), "s"(j < QA ? rA : rB), "s"(soff)
-                   : "m0");
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :
+                 : "s"(m0addr), "v"(voff[j]), "s"(j < QA ? rA : rB), "s"(soff)
+                 : "m0");
 #pragma clang diagnostic pop
-    }
+  };
+  auto dma = [&](int st, int kt) {
+#pragma unroll
+    for (int j = 0; j < Q; ++j) dma1(st, kt, j);
   };
   // Every wave waits for its own DMAs of the next tile (all but the (NS - 2) Q
   // youngest, or all of them near the end of K) and for its LDS reads; the
@@ -752,6 +756,25 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
         acc[i][j] = kTransposed<EPI> ? Mfma<T>::run(fb[slot][j], fa[slot][i], acc[i][j])
                                      : Mfma<T>::run(fa[slot][i], fb[slot][j], acc[i][j]);
   };
+  // the MFMAs of a k-step with DMA instructions j0 .. j0 + Q / 2 - 1 of a
+  // stage refill between them, evenly spaced, in this order
+  auto mfmas_dma = [&](int slot, int st, int kt, int j0) {
+    if constexpr (C::IL) {
+      constexpr int NM = FM * FN, ND = Q / 2, EVERY = NM / ND;
+      static_assert(Q % 2 == 0 && NM % ND == 0, "DMA spacing");
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        const int i = m / FN, j = m % FN;
+        acc[i][j] = kTransposed<EPI> ? Mfma<T>::run(fb[slot][j], fa[slot][i], acc[i][j])
+                                     : Mfma<T>::run(fa[slot][i], fb[slot][j], acc[i][j]);
+        if (m % EVERY == EVERY - 1) {
+          __builtin_amdgcn_sched_barrier(0);
+          dma1(st, kt, j0 + m / EVERY);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+  };
 
   // Tile t sits in stage t % NS. The loop starts at the barrier (whose
   // explicit lgkmcnt(0) leaves no LDS read pending at the loop header), then
@@ -768,7 +791,19 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
   if (NS - 1 < KT) dma(NS - 1, NS - 1);
   mfmas(0);
   int sc = 0;  // stage of tile t
-  for (int t = 0; t < KT - 1; ++t) {
+  int t = 0;
+  if constexpr (C::IL) {
+    for (; t < KT - NS; ++t) {
+      const int sn = sc + 1 == NS ? 0 : sc + 1;
+      sync(false);
+      load_frags(0, sn, 0);
+      mfmas_dma(1, sc, t + NS, 0);
+      load_frags(1, sn, 1);
+      mfmas_dma(0, sc, t + NS, Q / 2);
+      sc = sn;
+    }
+  }
+  for (; t < KT - 1; ++t) {
     const int sn = sc + 1 == NS ? 0 : sc + 1;
     sync(t + NS - 1 >= KT);
     load_frags(0, sn, 0);
@@ -1017,11 +1052,11 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
 //   single workgroup, so it gets 6 stages in flight.
 // - Otherwise 128 x 128 tiles with 3 stages, several workgroups per CU, so one
 //   workgroup's epilogue and barriers overlap another's MFMAs.
-using TileL = TileCfg<256, 256, 2, 4, 4>;   // 8 waves of 128 x 64, 128 KB LDS
-using TileW = TileCfg<256, 192, 2, 2, 5>;   // 4 waves of 128 x 96, 140 KB
-using TileM = TileCfg<192, 128, 2, 2, 6>;   // 4 waves of 96 x 64, 120 KB
-using TileS1 = TileCfg<128, 128, 2, 2, 6>;  // 4 waves of 64 x 64, 96 KB
-using TileS = TileCfg<128, 128, 2, 2, 3>;   // 4 waves of 64 x 64, 48 KB
+using TileL = TileCfg<256, 256, 2, 4, 4, true>;   // 8 waves of 128 x 64, 128 KB LDS
+using TileW = TileCfg<256, 192, 2, 2, 5>;         // 4 waves of 128 x 96, 140 KB
+using TileM = TileCfg<192, 128, 2, 2, 6>;         // 4 waves of 96 x 64, 120 KB
+using TileS1 = TileCfg<128, 128, 2, 2, 6, true>;  // 4 waves of 64 x 64, 96 KB
+using TileS = TileCfg<128, 128, 2, 2, 3, true>;   // 4 waves of 64 x 64, 48 KB
 
 template <typename T, int EPI>
 hipError_t dispatch_tiles(const GemmArgs& g, hipStream_t s) {

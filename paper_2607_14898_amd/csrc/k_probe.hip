@@ -8,7 +8,9 @@
 // accumulators, with operands that change every instruction (pseudo-random
 // values in [-1, 1), like real activations and weights), and records its
 // shader-clock cycles and wall-clock ticks. A second probe measures how many
-// bytes per clock the LDS of a compute unit delivers to ds_read_b128.
+// bytes per clock the LDS of a compute unit delivers to ds_read_b128, and a
+// third how far a wave's MFMAs and its vector instructions (exponentials,
+// fused multiply-adds) overlap.
 #include "fd_kernels.h"
 
 #include <hip/hip_bf16.h>
@@ -102,7 +104,79 @@ __global__ __launch_bounds__(512) void lds_read_kernel(int iters, unsigned long 
   }
 }
 
+// Issue overlap: per iteration 4 slots, each one 32x32x16 MFMA on its own
+// accumulator (MODE bit 0), then NEXP exponentials each followed by a multiply
+// (bit 1), then NVALU fused multiply-adds (bit 2), in this order (scheduling
+// barriers keep it); every vector instruction works on one of 16 independent
+// registers, so no slot waits on another slot's result.
+template <int MODE, int NEXP, int NVALU>
+__global__ __launch_bounds__(512) void overlap_kernel(int iters, unsigned long long* clk, float* sink) {
+  const int tid = threadIdx.x;
+  const float seed = 0.37f;
+  h16x8 a, b;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    a[e] = (_Float16)(seed * (tid + e));
+    b[e] = (_Float16)(seed * (tid - e));
+  }
+  f32x16p c[4];
+#pragma unroll
+  for (int m = 0; m < 4; ++m)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) c[m][r] = 0.f;
+  float x[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) x[i] = seed * (tid + i) * 1e-3f;
+  // the workgroup's time: from a common start until its last wave is done
+  // (waves sharing a SIMD do not progress at the same rate)
+  __syncthreads();
+  const unsigned long long c0 = clock64();
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      if (MODE & 1) c[m] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c[m], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (MODE & 2) {
+#pragma unroll
+        for (int e = 0; e < NEXP; ++e) x[(m * NEXP + e) & 15] = __builtin_amdgcn_exp2f(x[(m * NEXP + e) & 15]) * -0.5f;
+      }
+      if (MODE & 4) {
+#pragma unroll
+        for (int e = 0; e < NVALU; ++e) x[(m * NVALU + e + 7) & 15] = x[(m * NVALU + e + 7) & 15] * 0.999f + 0.001f;
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  float z = 0.f;
+#pragma unroll
+  for (int m = 0; m < 4; ++m)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) z += c[m][r];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z += x[i];
+  sink[blockIdx.x * blockDim.x + tid] = z;
+  __syncthreads();
+  const unsigned long long c1 = clock64();
+  if (tid == 0) clk[blockIdx.x] = c1 - c0;
+}
+
 }  // namespace
+
+hipError_t issue_overlap_probe(int mode, int blocks, int waves_per_simd, int iters, unsigned long long* clk,
+                               float* sink, hipStream_t s) {
+  if (blocks <= 0 || iters <= 0 || waves_per_simd < 1 || waves_per_simd > 2) return hipErrorInvalidValue;
+  const dim3 b(256 * waves_per_simd);
+  switch (mode) {
+    case 0: hipLaunchKernelGGL((overlap_kernel<1, 0, 0>), dim3(blocks), b, 0, s, iters, clk, sink); break;
+    case 1: hipLaunchKernelGGL((overlap_kernel<2, 4, 0>), dim3(blocks), b, 0, s, iters, clk, sink); break;
+    case 2: hipLaunchKernelGGL((overlap_kernel<3, 4, 0>), dim3(blocks), b, 0, s, iters, clk, sink); break;
+    case 3: hipLaunchKernelGGL((overlap_kernel<4, 0, 8>), dim3(blocks), b, 0, s, iters, clk, sink); break;
+    case 4: hipLaunchKernelGGL((overlap_kernel<5, 0, 8>), dim3(blocks), b, 0, s, iters, clk, sink); break;
+    case 5: hipLaunchKernelGGL((overlap_kernel<7, 4, 4>), dim3(blocks), b, 0, s, iters, clk, sink); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
 
 hipError_t lds_read_probe(int blocks, int iters, unsigned long long* clk, unsigned* sink, hipStream_t s) {
   if (blocks <= 0 || iters <= 0) return hipErrorInvalidValue;

@@ -93,6 +93,7 @@ def load_library() -> ctypes.CDLL:
                                        ctypes.POINTER(ctypes.c_double)]),
         "fd_measure_lds_bandwidth": (I32, [I32, P, ctypes.POINTER(ctypes.c_double),
                                            ctypes.POINTER(ctypes.c_double)]),
+        "fd_measure_issue_overlap": (I32, [I32, I32, P, ctypes.POINTER(ctypes.c_double)]),
         "fd_quantize_e4m3_rows": (I32, [P, I64, I64, P, P]),
         "fd_quantize_e4m3_rows_device": (I32, [P, I64, I64, P, P, P]),
         "fd_pack_e4m3_weight": (I32, [P, I64, I64, P]),
@@ -300,6 +301,17 @@ def fd_measure_lds_bandwidth(iters: int = 20000, stream=None):
     _check(load_library().fd_measure_lds_bandwidth(iters, _stream_handle(stream),
                                                    ctypes.byref(b), ctypes.byref(g)))
     return b.value, g.value
+
+
+ISSUE_OVERLAP_MODES = ("mfma", "exp4", "mfma+exp4", "fma8", "mfma+fma8", "mfma+exp4+fma4")
+
+
+def fd_measure_issue_overlap(waves_per_simd: int = 1, iters: int = 20000, stream=None):
+    """Shader cycles per slot and wave of the issue-overlap probe, keyed by
+    ISSUE_OVERLAP_MODES (a slot: one 32x32x16 MFMA and / or vector work)."""
+    c = (ctypes.c_double * 6)()
+    _check(load_library().fd_measure_issue_overlap(waves_per_simd, iters, _stream_handle(stream), c))
+    return dict(zip(ISSUE_OVERLAP_MODES, list(c)))
 
 
 def fd_measure_mfma_peak(dtype: str = "f16", iters: int = 100000, stream=None):

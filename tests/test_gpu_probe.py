@@ -27,3 +27,18 @@ def test_lds_bandwidth_probe_is_plausible():
     print(f"LDS read: {bpc:.1f} bytes per clock per CU at {ghz:.2f} GHz", flush=True)
     assert 32.0 <= bpc <= 1024.0
     assert 0.5 <= ghz <= 2.6
+
+
+def test_issue_overlap_probe_is_consistent():
+    """Cycles per slot of the MFMA / vector-instruction overlap probe: one
+    32x32x16 MFMA per slot takes at least the MFMA's 32 cycles with one wave per
+    SIMD (two waves share the matrix unit), and a slot with both kinds of work
+    takes at least as long as either kind alone and at most their sum (plus
+    a little issue slack)."""
+    for wps in (1, 2):
+        c = fdb.fd_measure_issue_overlap(wps, 2000)
+        print(wps, {k: round(v, 1) for k, v in c.items()}, flush=True)
+        assert 28.0 * wps <= c["mfma"] <= 64.0 * wps
+        for both, parts in (("mfma+exp4", ("mfma", "exp4")), ("mfma+fma8", ("mfma", "fma8"))):
+            assert c[both] >= 0.95 * max(c[p] for p in parts)
+            assert c[both] <= 1.1 * sum(c[p] for p in parts)

@@ -458,7 +458,7 @@ def main() -> int:
         },
         "kernel_classes": kclasses,
         "roofline": {
-            "kernel": "attn_mfma_kernel<f16, 4 heads, 64 queries/wave> (refinement-stack attention)",
+            "kernel": "attn_mfma_kernel<f16, 4 heads, 32 queries/wave> (refinement-stack attention)",
             "bound": "mfma",
             "achieved": round(achieved, 2),
             "peak": PEAK_F16_TFLOPS,

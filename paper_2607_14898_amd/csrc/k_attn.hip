@@ -8,7 +8,7 @@
 //
 // 16-bit path (D_h = 64): a workgroup is 4 wave64s; they are 4 query heads of
 // one KV group (GQA), so every K / V^T tile staged in LDS serves all four. Each
-// wave owns 64 queries as two 32-query MFMA blocks and computes S^T = K Q^T
+// wave owns NQB 32-query MFMA blocks (the launch uses one) and computes S^T = K Q^T
 // with the 32x32x16 MFMA, so a lane holds one query and 16 key scores per 32-key
 // block: the softmax max needs one cross-half exchange per tile and the row
 // sums stay lane-local until the end (per tile a packed-f16 sum of the f16
@@ -445,21 +445,16 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a, int q_tiles) {
 }  // namespace
 
 // Launch shape: 4 heads of a KV group per workgroup when the group has a
-// multiple of 4 query heads (GQA), and 64 queries per wave unless that leaves
-// the 256 CUs short of work (fewer than 1.5 rounds of two workgroups per CU);
-// then 32 queries per wave, which doubles the workgroups and fits three per CU.
+// multiple of 4 query heads (GQA), and 32 queries per wave: 143 registers let
+// three workgroups share a CU (three waves per SIMD), which hides more of the
+// per-tile latency than 64 queries per wave (239 registers, two per CU) saves
+// in LDS reads and barriers (measured: 2509 vs 2550 us per 720p refinement
+// launch; the same at 480p).
 template <typename TT, int HPB>
 hipError_t attn_launch(const AttnArgs& a, hipStream_t s) {
-  const int blocks64 = ((a.U + 64 * (4 / HPB) - 1) / (64 * (4 / HPB))) * a.n_units * a.B * (a.N / HPB);
-  if (blocks64 >= 768) {
-    const int q_tiles = (a.U + 64 * (4 / HPB) - 1) / (64 * (4 / HPB));
-    dim3 grid(q_tiles * a.n_units * a.B, a.N / HPB);
-    hipLaunchKernelGGL((attn_mfma_kernel<TT, HPB, 2>), grid, dim3(256), 0, s, a, q_tiles);
-  } else {
-    const int q_tiles = (a.U + 32 * (4 / HPB) - 1) / (32 * (4 / HPB));
-    dim3 grid(q_tiles * a.n_units * a.B, a.N / HPB);
-    hipLaunchKernelGGL((attn_mfma_kernel<TT, HPB, 1>), grid, dim3(256), 0, s, a, q_tiles);
-  }
+  const int q_tiles = (a.U + 32 * (4 / HPB) - 1) / (32 * (4 / HPB));
+  dim3 grid(q_tiles * a.n_units * a.B, a.N / HPB);
+  hipLaunchKernelGGL((attn_mfma_kernel<TT, HPB, 1>), grid, dim3(256), 0, s, a, q_tiles);
   return hipGetLastError();
 }
 

@@ -76,10 +76,17 @@ struct EpiParams {
   // fp16 SwiGLU / SiLU outputs beyond +-65504 are clamped to it; when set,
   // the number of clamped values is added here
   unsigned* sat = nullptr;
+  // 16-bit activation epilogues (EPI_STORE_ACT / _SILU / _GELU, EPI_SWIGLU of
+  // the 16-bit GEMM): write out_a in the packed operand layout (pack_a16_index
+  // with K = ld_out) instead of row-major
+  int out_packed = 0;
 };
 
 struct GemmArgs {
-  const void* A = nullptr;  // [M, K] row-major, lda
+  // [M, K] row-major with stride lda, or (16-bit MFMA GEMM, a_packed = 1)
+  // packed by pack_a16_index with lda = K over ceil(M / 16) 16 rows
+  const void* A = nullptr;
+  int a_packed = 0;
   // [N, K]: row-major with stride ldw for the fp32 GEMM; for the 16-bit MFMA
   // GEMM packed K-tile-major (see pack_w16_index), ldw = K
   const void* W = nullptr;
@@ -95,6 +102,14 @@ struct GemmArgs {
 inline int64_t pack_w16_index(int64_t row, int64_t k, int64_t K) {
   return ((row / 16) * (K / 32) + k / 32) * 512 + (row % 16) * 32 + k % 32;
 }
+// The same layout for a 16-bit activation [M, K] that is a GEMM's A operand.
+// Each DMA of a K tile then reads one contiguous 1 KB block (eight whole
+// 128-byte lines) instead of 16 rows of 64 bytes, which halves the L2
+// requests of the A side. Producers write it (norm, unshuffle, attention
+// output, activation epilogues); the buffer holds ceil(M / 16) 16 rows. The
+// GEMM reads the rows past M of the last block, which only reach output rows
+// that are not stored.
+inline int64_t pack_a16_index(int64_t row, int64_t k, int64_t K) { return pack_w16_index(row, k, K); }
 // Position of byte (row, k) of an [N, K] E4M3 weight in the packed layout the
 // FP8 MFMA GEMM reads: 1 KB blocks of 16 rows x 64 K-columns, block-row major,
 // rows padded with zeros to a multiple of 16.
@@ -102,7 +117,7 @@ inline int64_t pack_w8_index(int64_t row, int64_t k, int64_t K) {
   return ((row / 16) * (K / 64) + k / 64) * 1024 + (row % 16) * 64 + k % 64;
 }
 // 16-bit operand GEMM on MFMA (K > 0, K % 32 == 0, lda % 8 == 0, 16-byte aligned
-// A; W packed as above).
+// A, row-major or packed; W packed as above).
 hipError_t gemm_mfma(Act16 t, const GemmArgs& g, hipStream_t stream);
 // fp32 GEMM (any shape) for the fp32 compute path.
 hipError_t gemm_f32(const GemmArgs& g, hipStream_t stream);
@@ -117,7 +132,8 @@ struct AttnArgs {
   const void* q = nullptr;     // [rows, N * D_h], rows = B * n_units * U
   const void* k_ring = nullptr;// [B][G][S][U_pad][D_h]
   const void* vt_ring = nullptr;// [B][G][S][D_h][U_pad]
-  void* o = nullptr;           // [rows, N * D_h]
+  void* o = nullptr;           // [rows, N * D_h]; 16-bit path: packed (pack_a16_index) if o_packed
+  int o_packed = 0;
   int B = 1, N = 1, G = 1, Dh = 64;
   int U = 0, U_pad = 0;        // tokens per causal unit, padded to 64
   int S = 1;                   // ring slots
@@ -135,10 +151,11 @@ hipError_t attention_f32(const AttnArgs& a, hipStream_t stream);
 // (saturating), else with the per-row scale (rule of fd_quantize_e4m3_rows)
 // written to row_scale. amax_out, if set, is raised to the largest |output|
 // (fp32 bits; calibration).
+// packed: 16-bit output in the packed operand layout (pack_a16_index, K = D).
 hipError_t norm_rows(const float* x, int M, int D, const float* g, const float* b, int kind,
                      float eps, void* out, int out_kind, hipStream_t stream,
                      float* row_scale = nullptr, const float* static_sc = nullptr,
-                     unsigned* amax_out = nullptr);
+                     unsigned* amax_out = nullptr, bool packed = false);
 
 // Per-row E4M3 quantisation (rule of fd_quantize_e4m3_rows) of in [M, K]
 // (in_kind 0 f16, 2 fp32) into codes [M, K] bytes and scale [M] fp32;
@@ -153,9 +170,10 @@ hipError_t qkv_post(const QkvPostArgs& a, hipStream_t stream);
 // stack and call, before the QKV post step of its layers.
 hipError_t rope_time(const QkvPostArgs& a, hipStream_t stream);
 
-// PixelUnshuffle + flatten of latent frames into embedding operands [B F L, K_pad].
+// PixelUnshuffle + flatten of latent frames into embedding operands [B F L, K_pad]
+// (packed: 16-bit output in the packed operand layout, K = K_pad).
 hipError_t unshuffle_latent(const void* z, int z_kind, int B, int C, int F, int H, int W, int p,
-                            int K_pad, void* u, int out_kind, hipStream_t stream);
+                            int K_pad, void* u, int out_kind, hipStream_t stream, bool packed = false);
 
 // h[m, j] = SiLU(raw[m, j]) * raw[m, H + j]  (fp32 path, un-interleaved weights)
 hipError_t swiglu_f32(const float* raw, int M, int H, float* h, hipStream_t stream);

@@ -366,7 +366,17 @@ struct Ctx {
   bool calibrate = false;  // FP8 MLP: per-token scales, maxima recorded into dec->calib
 };
 
-fd_status run_gemm(Ctx& x, const fd::GemmArgs& g, double algo_k) {
+fd_status run_gemm(Ctx& x, const fd::GemmArgs& g_in, double algo_k) {
+  fd::GemmArgs g = g_in;
+  if (x.dec->d.is16) {
+    // On the 16-bit path every A operand of these GEMMs (norm, unshuffle and
+    // attention outputs, the hidden of the activation epilogues) is stored in
+    // the packed operand layout, and so is every 16-bit activation output.
+    g.a_packed = 1;
+    if (g.epi == fd::EPI_SWIGLU || g.epi == fd::EPI_STORE_ACT || g.epi == fd::EPI_STORE_SILU ||
+        g.epi == fd::EPI_STORE_GELU)
+      g.ep.out_packed = 1;
+  }
   hipEvent_t ev;
   fd_status st = probe_begin(x.c, FD_KC_GEMM, x.s, &ev);
   if (st) return st;
@@ -403,7 +413,7 @@ fd_status run_norm(Ctx& x, const float* src, int M, const float* g, const float*
   hipError_t e = e4m3 ? fd::norm_rows(src, M, dec->cfg.dim, g, b, dec->cfg.norm_kind, dec->cfg.norm_eps,
                                       x.c->a8, 3, x.s, x.c->sa, static_sc, amax_out)
                       : fd::norm_rows(src, M, dec->cfg.dim, g, b, dec->cfg.norm_kind, dec->cfg.norm_eps,
-                                      x.c->a, dec->d.act_kind, x.s);
+                                      x.c->a, dec->d.act_kind, x.s, nullptr, nullptr, nullptr, dec->d.is16);
   if (e != hipSuccess) return fail(FD_ERR_DEVICE, "norm launch failed: %s", hipGetErrorString(e));
   return probe_end(x.c, x.s, ev, (double)M * dec->cfg.dim * (4.0 + (e4m3 ? 1.0 : dec->d.act_bytes)));
 }
@@ -508,6 +518,7 @@ fd_status run_stack(Ctx& x, const std::vector<LayerW>& layers, float* xs, int ro
     aa.u0 = u0;
     aa.window = c.window;
     aa.scale = 1.0f / std::sqrt((float)d.Dh);
+    aa.o_packed = d.is16 ? 1 : 0;  // the O projection's A operand
     double keys = 0.0;  // visible keys summed over the call's query units
     for (int lu = 0; lu < n_units; ++lu) {
       const int64_t u = u0 + lu;
@@ -649,7 +660,7 @@ fd_status decode(const fd_decoder* dec, const void* latent, int32_t latent_dtype
     if ((st = probe_begin(kc, FD_KC_EMBED_IN, s, &ev))) break;
     hipError_t e = fd::unshuffle_latent(latent, latent_dtype == FD_DTYPE_F32 ? 0 : (latent_dtype == FD_DTYPE_BF16 ? 1 : 2),
                                         B, c.latent_channels, F, c.latent_h, c.latent_w, c.patch,
-                                        d.K_pad, kc->u, d.act_kind, s);
+                                        d.K_pad, kc->u, d.act_kind, s, d.is16);
     if (e != hipSuccess) { st = fail(FD_ERR_DEVICE, "unshuffle launch failed: %s", hipGetErrorString(e)); break; }
     if ((st = probe_end(kc, s, ev, (double)M * d.K_in * (latent_dtype == FD_DTYPE_F32 ? 4 : 2) +
                                        (double)M * d.K_pad * d.act_bytes))) break;
@@ -946,15 +957,17 @@ WsLayout ws_layout(const fd_config& c, const Derived& d, int64_t M) {
   const int64_t raw_cols = d.is16 ? 0 : std::max<int64_t>(d.qkv_w, 2 * c.mlp_hidden);
   const int64_t hid = std::max<int64_t>(c.mlp_hidden, tf ? c.head_hidden : 0);
   auto al = [](int64_t b) { return (size_t)((b + 255) / 256 * 256); };
+  // GEMM operands (a, o, h, u) in the packed layout hold whole 16-row blocks
+  const int64_t M16 = (M + 15) / 16 * 16, MR16 = (MR + 15) / 16 * 16;
   const size_t sizes[13] = {
       al(M * D * 4),                                           // x_bb
       tf ? al(MR * D * 4) : 0,                                 // x_rf
       al(MR * raw_cols * 4),                                   // raw
-      al(MR * D * (int64_t)es),                                // a
+      al(MR16 * D * (int64_t)es),                              // a
       al(MR * D * (int64_t)es),                                // q
-      al(MR * D * (int64_t)es),                                // o
-      al(MR * hid * (int64_t)es),                              // h
-      al(M * d.K_pad * (int64_t)es),                           // u
+      al(MR16 * D * (int64_t)es),                              // o
+      al(MR16 * hid * (int64_t)es),                            // h
+      al(M16 * d.K_pad * (int64_t)es),                         // u
       al((int64_t)(M / d.L) * c.r_t * (d.Dh / 2) * (int64_t)sizeof(float2)),  // rope_t
       d.mlp8 ? al(MR * D) : 0,                                 // a8
       d.mlp8 ? al(MR * c.mlp_hidden) : 0,                      // h8

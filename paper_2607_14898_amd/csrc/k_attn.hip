@@ -366,7 +366,12 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
     const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
     const float inv = 1.f / l_tot;
     if (q0 + qb * 32 + lr < a.U) {
-      T* op = (T*)a.o + qrow(qb) * ldq + n * 64;
+      // row-major, or the O projection's packed operand layout (blocks of 16
+      // rows x 32 columns; the head's two 32-column halves are blocks 2n, 2n + 1)
+      const int64_t orow = qrow(qb);
+      T* op = (T*)a.o + (a.o_packed ? (orow >> 4) * ldq * 16 + (orow & 15) * 32 + (int64_t)n * 1024
+                                    : orow * ldq + n * 64);
+      const int dstep = a.o_packed ? 512 : 32;
 #pragma unroll
       for (int d = 0; d < 2; ++d)
 #pragma unroll
@@ -375,7 +380,7 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
           E o4[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) o4[e] = M::cvt(acc[qb][d][r4 * 4 + e] * inv);
-          *reinterpret_cast<uint2*>(op + d * 32 + 8 * r4 + 4 * lh) = *reinterpret_cast<uint2*>(o4);
+          *reinterpret_cast<uint2*>(op + d * dstep + 8 * r4 + 4 * lh) = *reinterpret_cast<uint2*>(o4);
         }
     }
   }
@@ -473,7 +478,7 @@ hipError_t attention_mfma(Act16 t, const AttnArgs& a, hipStream_t s) {
 }
 
 hipError_t attention_f32(const AttnArgs& a, hipStream_t s) {
-  if (a.U <= 0 || a.U_pad % 64 || a.N % a.G) return hipErrorInvalidValue;
+  if (a.U <= 0 || a.U_pad % 64 || a.N % a.G || a.o_packed) return hipErrorInvalidValue;
   const int q_tiles = (a.U + 63) / 64;
   dim3 grid(q_tiles * a.n_units * a.B, a.N);
   switch (a.Dh) {

@@ -67,7 +67,13 @@ __device__ __forceinline__ void count_sat(unsigned* sat, int n) {
 // offset splits into a part that depends only on the output row and a part
 // that depends only on the column, so the per-element cost is one add. The
 // reshapes of the temporal upsampling (Eq. temporal_upsample) and of the
-// PixelShuffle store (Sec. 3.4 Step 3) are expressed this way.
+// PixelShuffle store (Sec. 3.4 Step 3) are expressed this way, and so is the
+// packed operand layout of 16-bit activations (blocks of 16 rows x 32
+// columns: row part (row / 16) 16 ld + (row % 16) 32, column part
+// (col / 32) 512 + col % 32).
+template <int EPI>
+constexpr bool kPackable = EPI == EPI_SWIGLU || EPI == EPI_STORE_ACT || EPI == EPI_STORE_SILU ||
+                           EPI == EPI_STORE_GELU;
 template <int EPI>
 __device__ __forceinline__ int64_t row_off(const EpiParams& p, int row) {
   if constexpr (EPI == EPI_TUP) {
@@ -89,6 +95,8 @@ __device__ __forceinline__ int64_t row_off(const EpiParams& p, int row) {
     }
     return ((int64_t)b * p.C * p.frames_out + fo) * OHW + (int64_t)p.s * h * OW + p.s * w;
   } else {
+    if constexpr (kPackable<EPI>)
+      if (p.out_packed) return (int64_t)(row >> 4) * p.ld_out * 16 + (row & 15) * 32;
     return (int64_t)row * p.ld_out;
   }
 }
@@ -111,6 +119,8 @@ __device__ __forceinline__ int64_t col_off(const EpiParams& p, int col) {
     const int i1 = rem / p.s, i2 = rem - i1 * p.s;
     return ((int64_t)c3 * p.frames_out + j) * OHW + (int64_t)i1 * OW + i2;
   } else {
+    if constexpr (kPackable<EPI>)
+      if (p.out_packed) return (int64_t)(col >> 5) * 512 + (col & 31);
     return col;
   }
 }
@@ -521,7 +531,8 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
             *reinterpret_cast<int*>((uint8_t*)ep.out_a + ro[i] + oc) = w;
             continue;
           }
-          *reinterpret_cast<uint2*>((T*)ep.out_a + ro[i] + oc) = *reinterpret_cast<const uint2*>(o4);
+          *reinterpret_cast<uint2*>((T*)ep.out_a + ro[i] + col_off<EPI>(ep, oc)) =
+              *reinterpret_cast<const uint2*>(o4);
         }
       }
   } else {
@@ -656,7 +667,7 @@ template <int EPI> constexpr bool kTransposed = EPI == EPI_SWIGLU || EPI == EPI_
 template <typename T, class C, int EPI>
 __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
     const T* __restrict__ A, const T* __restrict__ W, int M, int N, int K, int lda, int ldw,
-    EpiParams ep, int tiles_m, int tiles_n, int vec_store) {
+    EpiParams ep, int tiles_m, int tiles_n, int vec_store, int a_packed) {
   constexpr int BM = C::BM, BN = C::BN, FM = C::FM, FN = C::FN, NS = C::NS, NW = C::NW;
   constexpr int QA = C::QA, Q = C::QA + C::QB, STAGE = C::STAGE;
   using V = typename Mfma<T>::V;
@@ -669,13 +680,17 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
   const int m0 = tm * BM, n0 = tn * BN;
   const int wm0 = (wave / C::WAVES_N) * C::WM, wn0 = (wave % C::WAVES_N) * C::WN;
 
-  // A is row-major (lda). W is packed K-tile-major: blocks of 16 rows x 32
-  // K-columns (1 KB), block (row / 16, k / 32) at ((row / 16) (K / 32) + k / 32) KB,
-  // rows padded with zeros to a multiple of 16, so each DMA of W reads one
-  // contiguous 1 KB block.
+  // W is packed K-tile-major: blocks of 16 rows x 32 K-columns (1 KB), block
+  // (row / 16, k / 32) at ((row / 16) (K / 32) + k / 32) KB, rows padded with
+  // zeros to a multiple of 16, so each DMA of W reads one contiguous 1 KB
+  // block. A is row-major (lda), or packed the same way (lda = K, whole
+  // 16-row blocks readable).
   const int KB = K / BKD;  // K tiles
+  const bool apk = a_packed != 0;
+  const int a_rows = apk ? (min(BM, M - m0) + 15) / 16 * 16 : min(BM, M - m0);
   const __amdgpu_buffer_rsrc_t rA =
-      make_rsrc(A + (int64_t)m0 * lda, (uint32_t)min(BM, M - m0) * lda * (uint32_t)sizeof(T));
+      make_rsrc(A + (int64_t)m0 * lda, (uint32_t)a_rows * lda * (uint32_t)sizeof(T));
+  const uint32_t a_kstep = apk ? 1024u : (uint32_t)BKD * (uint32_t)sizeof(T);  // bytes per K tile
   const int nrows_w = min(BN, (N + 15) / 16 * 16 - n0);
   const __amdgpu_buffer_rsrc_t rB =
       make_rsrc(W + (int64_t)(n0 / 16) * KB * 512, (uint32_t)(nrows_w / 16) * KB * 1024u);
@@ -688,13 +703,14 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_mfma_kernel(
 #pragma unroll
   for (int j = 0; j < Q; ++j) {
     const int q = j * NW + wave;
-    voff[j] = j < QA ? (uint32_t)((16 * q + lrow) * lda + lchunk * 8) * (uint32_t)sizeof(T)
-                     : (uint32_t)(q - BM / 16) * KB * 1024u + (uint32_t)(lrow * 64 + lchunk * 16);
+    voff[j] = j >= QA ? (uint32_t)(q - BM / 16) * KB * 1024u + (uint32_t)(lrow * 64 + lchunk * 16)
+              : apk   ? (uint32_t)q * KB * 1024u + (uint32_t)(lrow * 64 + lchunk * 16)
+                      : (uint32_t)((16 * q + lrow) * lda + lchunk * 8) * (uint32_t)sizeof(T);
   }
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint4*)lds;
   // DMA instruction j of the refill of stage st with K tile kt
   auto dma1 = [&](int st, int kt, int j) {
-    const uint32_t soff = j < QA ? (uint32_t)kt * BKD * (uint32_t)sizeof(T) : (uint32_t)kt * 1024u;
+    const uint32_t soff = j < QA ? (uint32_t)kt * a_kstep : (uint32_t)kt * 1024u;
     const uint32_t m0addr = lds0 + (uint32_t)(st * STAGE + 64 * (j * NW + wave)) * 16u;
     // M0 is reserved by the compiler, but nothing else in this kernel reads it
     // (no LDS DMA builtins, interpolation, GWS or message sends).
@@ -1037,7 +1053,8 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   if (EPI == EPI_TUP) vec = vec && g.ep.dim % 4 == 0;
   vec = vec && ((uintptr_t)g.ep.out_f % 16 == 0) && ((uintptr_t)g.ep.out_a % 8 == 0);
   hipLaunchKernelGGL((gemm_mfma_kernel<T, C, EPI>), dim3(tm * tn), dim3(C::NT), 0, s,
-                     (const T*)g.A, (const T*)g.W, g.M, g.N, g.K, g.lda, g.ldw, g.ep, tm, tn, vec ? 1 : 0);
+                     (const T*)g.A, (const T*)g.W, g.M, g.N, g.K, g.lda, g.ldw, g.ep, tm, tn, vec ? 1 : 0,
+                     g.a_packed);
   return hipGetLastError();
 }
 
@@ -1071,8 +1088,9 @@ hipError_t dispatch_tiles(const GemmArgs& g, hipStream_t s) {
     // are fewer than those of 256 x 256 tiles (for instance 342 -> 456 tiles,
     // 2 -> 1.5 round-equivalents, for 14400 x 1536 outputs). Their 96-column
     // wave blocks suit every epilogue but the paired SwiGLU and the QKV post
-    // step (one 64-column head vector per wave).
-    if constexpr (EPI != EPI_SWIGLU && EPI != EPI_QKV) {
+    // step (one 64-column head vector per wave); the GELU epilogue's erf needs
+    // more registers than a 4-wave 256 x 192 tile leaves.
+    if constexpr (EPI != EPI_SWIGLU && EPI != EPI_QKV && EPI != EPI_STORE_GELU) {
       const int rounds_l = (tiles(256, 256) + 255) / 256, rounds_w = (tiles(256, 192) + 255) / 256;
       if (4 * rounds_w * 3 < 4 * rounds_l * 4) return launch_gemm<T, TileW, EPI>(g, s);
     }
@@ -1180,6 +1198,7 @@ hipError_t dispatch_fp8(const GemmArgs& g, hipStream_t s) {
 
 hipError_t gemm_fp8(const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  if (g.a_packed || g.ep.out_packed) return hipErrorInvalidValue;  // row-major codes and outputs
   if (g.K <= 0 || g.K % 64 || g.lda % 16 || !g.ep.row_scale || !g.ep.col_scale) return hipErrorInvalidValue;
   if (g.epi == EPI_SWIGLU) {
     if (g.N % 64 || g.ep.ld_out % 4 || (uintptr_t)g.ep.out_a % 8) return hipErrorInvalidValue;
@@ -1196,6 +1215,10 @@ hipError_t gemm_fp8(const GemmArgs& g, hipStream_t s) {
 hipError_t gemm_mfma(Act16 t, const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
   if (g.K <= 0 || g.K % BKD || g.lda % 8 || g.ldw != g.K) return hipErrorInvalidValue;
+  if (g.a_packed && g.lda != g.K) return hipErrorInvalidValue;
+  if (g.ep.out_packed && (g.ep.ld_out % 32 || !(g.epi == EPI_SWIGLU || g.epi == EPI_STORE_ACT ||
+                                                g.epi == EPI_STORE_SILU || g.epi == EPI_STORE_GELU)))
+    return hipErrorInvalidValue;
   if ((g.epi == EPI_SWIGLU || g.epi == EPI_QKV) && g.N % 64) return hipErrorInvalidValue;
   if (g.epi == EPI_QKV && g.ep.qkv.Dh != 64) return hipErrorInvalidValue;
   return t == Act16::F16 ? dispatch_epi<_Float16>(g, s) : dispatch_epi<__hip_bfloat16>(g, s);
@@ -1203,6 +1226,7 @@ hipError_t gemm_mfma(Act16 t, const GemmArgs& g, hipStream_t s) {
 
 hipError_t gemm_f32(const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  if (g.a_packed || g.ep.out_packed) return hipErrorInvalidValue;  // row-major fp32 operands
   switch (g.epi) {
     case EPI_STORE_F32: return launch_f32<EPI_STORE_F32>(g, s);
     case EPI_RESID_ADD: return launch_f32<EPI_RESID_ADD>(g, s);

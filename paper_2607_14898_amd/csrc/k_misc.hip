@@ -22,6 +22,12 @@ __device__ __forceinline__ void store_kind(void* out, int64_t i, float v, int ki
   else ((float*)out)[i] = v;
 }
 
+// Element (row, k) of a 16-bit [rows, K] activation in the packed operand
+// layout of the MFMA GEMM (blocks of 16 rows x 32 columns, block-row major).
+__device__ __forceinline__ int64_t pk16(int64_t row, int k, int K) {
+  return ((row >> 4) * (K >> 5) + (k >> 5)) * 512 + (row & 15) * 32 + (k & 31);
+}
+
 // Four consecutive values as one 8-byte (16-bit kinds) or 16-byte (fp32) store.
 __device__ __forceinline__ void store4(void* out, int64_t i, float4 y, int kind) {
   if (kind == 0) {
@@ -78,7 +84,7 @@ __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, 
                                                    const float* __restrict__ bta, float eps,
                                                    void* out, int out_kind, float* row_scale,
                                                    const float* __restrict__ static_sc,
-                                                   unsigned* __restrict__ amax_out) {
+                                                   unsigned* __restrict__ amax_out, int packed) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
@@ -130,7 +136,7 @@ __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, 
         v[i] = y;
         amax = fmaxf(fmaxf(amax, fmaxf(fabsf(y.x), fabsf(y.y))), fmaxf(fabsf(y.z), fabsf(y.w)));
       } else {
-        store4(out, (int64_t)row * D + 4 * c, y, out_kind);
+        store4(out, packed ? pk16(row, 4 * c, D) : (int64_t)row * D + 4 * c, y, out_kind);
       }
     }
   }
@@ -292,7 +298,7 @@ __global__ void rope_time_kernel(int64_t tau0, int n_fs, int np, const int* axis
 // u[(b F + f) L + h W_t + w, c p^2 + i p + j] = z[b, c, f, p h + i, p w + j]; zero padding to K_pad.
 __global__ __launch_bounds__(256) void unshuffle_kernel(const void* z, int z_kind, int B, int C,
                                                         int F, int H, int W, int p, int K_pad,
-                                                        void* u, int out_kind) {
+                                                        void* u, int out_kind, int packed) {
   const int Ht = H / p, Wt = W / p, L = Ht * Wt;
   const int64_t total = (int64_t)B * F * L * K_pad;
   for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total;
@@ -311,7 +317,7 @@ __global__ __launch_bounds__(256) void unshuffle_kernel(const void* z, int z_kin
       else if (z_kind == 1) v = __bfloat162float(((const __hip_bfloat16*)z)[zi]);
       else v = (float)((const _Float16*)z)[zi];
     }
-    store_kind(u, e, v, out_kind);
+    store_kind(u, packed ? pk16(row, k, K_pad) : e, v, out_kind);
   }
 }
 
@@ -342,16 +348,17 @@ int grid_for(int64_t total) {
 
 hipError_t norm_rows(const float* x, int M, int D, const float* g, const float* b, int kind,
                      float eps, void* out, int out_kind, hipStream_t s, float* row_scale,
-                     const float* static_sc, unsigned* amax_out) {
+                     const float* static_sc, unsigned* amax_out, bool packed) {
   if (M <= 0) return hipSuccess;
   if (D % 4 || D > 2048 || (out_kind == 3 && !row_scale && !static_sc)) return hipErrorInvalidValue;
+  if (packed && (D % 32 || (out_kind != 0 && out_kind != 1))) return hipErrorInvalidValue;
   const int grid = (M + 3) / 4;
   if (kind == 0)
     hipLaunchKernelGGL(norm_kernel<0>, dim3(grid), dim3(256), 0, s, x, M, D, g, b, eps, out, out_kind,
-                       row_scale, static_sc, amax_out);
+                       row_scale, static_sc, amax_out, packed ? 1 : 0);
   else
     hipLaunchKernelGGL(norm_kernel<1>, dim3(grid), dim3(256), 0, s, x, M, D, g, b, eps, out, out_kind,
-                       row_scale, static_sc, amax_out);
+                       row_scale, static_sc, amax_out, packed ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -391,10 +398,11 @@ hipError_t qkv_post(const QkvPostArgs& a, hipStream_t s) {
 }
 
 hipError_t unshuffle_latent(const void* z, int z_kind, int B, int C, int F, int H, int W, int p,
-                            int K_pad, void* u, int out_kind, hipStream_t s) {
+                            int K_pad, void* u, int out_kind, hipStream_t s, bool packed) {
+  if (packed && (K_pad % 32 || (out_kind != 0 && out_kind != 1))) return hipErrorInvalidValue;
   const int64_t total = (int64_t)B * F * (H / p) * (W / p) * K_pad;
   hipLaunchKernelGGL(unshuffle_kernel, dim3(grid_for(total)), dim3(256), 0, s, z, z_kind, B, C, F,
-                     H, W, p, K_pad, u, out_kind);
+                     H, W, p, K_pad, u, out_kind, packed ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -77,8 +77,9 @@ struct EpiParams {
   // the number of clamped values is added here
   unsigned* sat = nullptr;
   // 16-bit activation epilogues (EPI_STORE_ACT / _SILU / _GELU, EPI_SWIGLU of
-  // the 16-bit GEMM): write out_a in the packed operand layout (pack_a16_index
-  // with K = ld_out) instead of row-major
+  // the 16-bit GEMM) and the E4M3 SwiGLU codes of the FP8 GEMM: write out_a in
+  // the packed operand layout (pack_a16_index / pack_a8_index with K = ld_out)
+  // instead of row-major
   int out_packed = 0;
 };
 
@@ -116,13 +117,17 @@ inline int64_t pack_a16_index(int64_t row, int64_t k, int64_t K) { return pack_w
 inline int64_t pack_w8_index(int64_t row, int64_t k, int64_t K) {
   return ((row / 16) * (K / 64) + k / 64) * 1024 + (row % 16) * 64 + k % 64;
 }
+// The same layout for E4M3 activation codes that are an FP8 GEMM's A operand
+// (a_packed; written by the norm, the quantiser and the E4M3 SwiGLU epilogue).
+inline int64_t pack_a8_index(int64_t row, int64_t k, int64_t K) { return pack_w8_index(row, k, K); }
 // 16-bit operand GEMM on MFMA (K > 0, K % 32 == 0, lda % 8 == 0, 16-byte aligned
 // A, row-major or packed; W packed as above).
 hipError_t gemm_mfma(Act16 t, const GemmArgs& g, hipStream_t stream);
 // fp32 GEMM (any shape) for the fp32 compute path.
 hipError_t gemm_f32(const GemmArgs& g, hipStream_t stream);
 // E4M3 x E4M3 GEMM on the gfx950 32x32x64 FP8 MFMA: A [M, K] E4M3 bytes
-// row-major (lda bytes, lda % 16 == 0), W packed by pack_w8_index, K % 64 == 0;
+// row-major (lda bytes, lda % 16 == 0) or packed (a_packed, pack_a8_index),
+// W packed by pack_w8_index, K % 64 == 0;
 // epilogues EPI_SWIGLU (fp16 out_a), EPI_SWIGLU_E4M3 (E4M3 out_a) and
 // EPI_RESID_ADD, after the row / column scales of EpiParams.
 hipError_t gemm_fp8(const GemmArgs& g, hipStream_t stream);
@@ -151,7 +156,8 @@ hipError_t attention_f32(const AttnArgs& a, hipStream_t stream);
 // (saturating), else with the per-row scale (rule of fd_quantize_e4m3_rows)
 // written to row_scale. amax_out, if set, is raised to the largest |output|
 // (fp32 bits; calibration).
-// packed: 16-bit output in the packed operand layout (pack_a16_index, K = D).
+// packed: output in the packed operand layout (16-bit: pack_a16_index; E4M3
+// codes: pack_a8_index; K = D).
 hipError_t norm_rows(const float* x, int M, int D, const float* g, const float* b, int kind,
                      float eps, void* out, int out_kind, hipStream_t stream,
                      float* row_scale = nullptr, const float* static_sc = nullptr,
@@ -159,9 +165,11 @@ hipError_t norm_rows(const float* x, int M, int D, const float* g, const float* 
 
 // Per-row E4M3 quantisation (rule of fd_quantize_e4m3_rows) of in [M, K]
 // (in_kind 0 f16, 2 fp32) into codes [M, K] bytes and scale [M] fp32;
-// amax_out as for norm_rows.
+// amax_out as for norm_rows; packed: codes in the FP8 GEMM's packed operand
+// layout (pack_a8_index, K % 64 == 0).
 hipError_t quant_rows_e4m3(const void* in, int in_kind, int64_t M, int K, uint8_t* codes,
-                           float* scale, hipStream_t stream, unsigned* amax_out = nullptr);
+                           float* scale, hipStream_t stream, unsigned* amax_out = nullptr,
+                           bool packed = false);
 
 // Split raw qkv (fp32, bias included) into rotated queries and the KV ring
 // (KV-norm, RoPE) for rows of one call.

@@ -411,14 +411,19 @@ fd_status run_norm(Ctx& x, const float* src, int M, const float* g, const float*
   fd_status st = probe_begin(x.c, FD_KC_NORM, x.s, &ev);
   if (st) return st;
   hipError_t e = e4m3 ? fd::norm_rows(src, M, dec->cfg.dim, g, b, dec->cfg.norm_kind, dec->cfg.norm_eps,
-                                      x.c->a8, 3, x.s, x.c->sa, static_sc, amax_out)
+                                      x.c->a8, 3, x.s, x.c->sa, static_sc, amax_out, true)
                       : fd::norm_rows(src, M, dec->cfg.dim, g, b, dec->cfg.norm_kind, dec->cfg.norm_eps,
                                       x.c->a, dec->d.act_kind, x.s, nullptr, nullptr, nullptr, dec->d.is16);
   if (e != hipSuccess) return fail(FD_ERR_DEVICE, "norm launch failed: %s", hipGetErrorString(e));
   return probe_end(x.c, x.s, ev, (double)M * dec->cfg.dim * (4.0 + (e4m3 ? 1.0 : dec->d.act_bytes)));
 }
 
-fd_status run_gemm8(Ctx& x, const fd::GemmArgs& g, double algo_k) {
+fd_status run_gemm8(Ctx& x, const fd::GemmArgs& g_in, double algo_k) {
+  // the E4M3 A operands (norm and quantiser codes, the E4M3 SwiGLU codes) are
+  // stored in the FP8 GEMM's packed operand layout
+  fd::GemmArgs g = g_in;
+  g.a_packed = 1;
+  if (g.epi == fd::EPI_SWIGLU_E4M3) g.ep.out_packed = 1;
   hipEvent_t ev;
   fd_status st = probe_begin(x.c, FD_KC_GEMM, x.s, &ev);
   if (st) return st;
@@ -575,7 +580,7 @@ fd_status run_stack(Ctx& x, const std::vector<LayerW>& layers, float* xs, int ro
       g.ep.col_scale = w.s1;
       if ((st = run_gemm8(x, g, D))) return st;
       if ((st = probe_begin(kc, FD_KC_NORM, x.s, &ev))) return st;
-      e = fd::quant_rows_e4m3(kc->h, 0, rows, H, kc->h8, kc->sh, x.s, cal ? cal + 1 : nullptr);
+      e = fd::quant_rows_e4m3(kc->h, 0, rows, H, kc->h8, kc->sh, x.s, cal ? cal + 1 : nullptr, true);
       if (e != hipSuccess) return fail(FD_ERR_DEVICE, "quantisation launch failed: %s", hipGetErrorString(e));
       if ((st = probe_end(kc, x.s, ev, (double)rows * H * 3.0))) return st;
       g = gemm_args(kc->h8, H, w.w2, rows, D, H, fd::EPI_RESID_ADD, w.b2);
@@ -957,7 +962,7 @@ WsLayout ws_layout(const fd_config& c, const Derived& d, int64_t M) {
   const int64_t raw_cols = d.is16 ? 0 : std::max<int64_t>(d.qkv_w, 2 * c.mlp_hidden);
   const int64_t hid = std::max<int64_t>(c.mlp_hidden, tf ? c.head_hidden : 0);
   auto al = [](int64_t b) { return (size_t)((b + 255) / 256 * 256); };
-  // GEMM operands (a, o, h, u) in the packed layout hold whole 16-row blocks
+  // GEMM operands (a, o, h, u, a8, h8) in the packed layout hold whole 16-row blocks
   const int64_t M16 = (M + 15) / 16 * 16, MR16 = (MR + 15) / 16 * 16;
   const size_t sizes[13] = {
       al(M * D * 4),                                           // x_bb
@@ -969,8 +974,8 @@ WsLayout ws_layout(const fd_config& c, const Derived& d, int64_t M) {
       al(MR16 * hid * (int64_t)es),                            // h
       al(M16 * d.K_pad * (int64_t)es),                         // u
       al((int64_t)(M / d.L) * c.r_t * (d.Dh / 2) * (int64_t)sizeof(float2)),  // rope_t
-      d.mlp8 ? al(MR * D) : 0,                                 // a8
-      d.mlp8 ? al(MR * c.mlp_hidden) : 0,                      // h8
+      d.mlp8 ? al(MR16 * D) : 0,                               // a8
+      d.mlp8 ? al(MR16 * c.mlp_hidden) : 0,                    // h8
       d.mlp8 ? al(MR * 4) : 0,                                 // sa
       d.mlp8 ? al(MR * 4) : 0};                                // sh
   WsLayout w;

@@ -528,7 +528,13 @@ __device__ __forceinline__ void store_tile_t(const EpiParams& ep, const f32x16 (
             auto cl = [&](float v) { return fminf(448.f, fmaxf(-448.f, v * q_inv)); };
             int w = __builtin_amdgcn_cvt_pk_fp8_f32(cl(h4[0]), cl(h4[1]), 0, false);
             w = __builtin_amdgcn_cvt_pk_fp8_f32(cl(h4[2]), cl(h4[3]), w, true);
-            *reinterpret_cast<int*>((uint8_t*)ep.out_a + ro[i] + oc) = w;
+            // E4M3 codes: row-major, or the FP8 GEMM's packed operand layout
+            // (blocks of 16 rows x 64 bytes)
+            const int64_t rr = r0 + i * 32 + lr;
+            const int64_t bo = ep.out_packed ? (rr >> 4) * ep.ld_out * 16 + (rr & 15) * 64 +
+                                                   (int64_t)(oc >> 6) * 1024 + (oc & 63)
+                                             : ro[i] + oc;
+            *reinterpret_cast<int*>((uint8_t*)ep.out_a + bo) = w;
             continue;
           }
           *reinterpret_cast<uint2*>((T*)ep.out_a + ro[i] + col_off<EPI>(ep, oc)) =
@@ -872,7 +878,7 @@ __device__ __forceinline__ f32x16 mfma_e4m3(i32x8 a, i32x8 b, f32x16 c) {
 template <class C, int EPI>
 __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_fp8_kernel(
     const uint8_t* __restrict__ A, const uint8_t* __restrict__ W, int M, int N, int K, int lda,
-    EpiParams ep, int tiles_m, int tiles_n) {
+    EpiParams ep, int tiles_m, int tiles_n, int a_packed) {
   constexpr int BM = C::BM, BN = C::BN, FM = C::FM, FN = C::FN, NS = C::NS, NW = C::NW;
   constexpr int QA = C::QA, Q = C::QA + C::QB, STAGE = C::STAGE;
   constexpr bool TR = kTransposed<EPI>;
@@ -886,7 +892,10 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_fp8_kernel(
   const int wm0 = (wave / C::WAVES_N) * C::WM, wn0 = (wave % C::WAVES_N) * C::WN;
 
   const int KB = K / 64;  // K tiles (64-byte stage rows)
-  const __amdgpu_buffer_rsrc_t rA = make_rsrc(A + (int64_t)m0 * lda, (uint32_t)min(BM, M - m0) * (uint32_t)lda);
+  // A row-major (lda bytes), or packed like W (lda = K, whole 16-row blocks)
+  const bool apk = a_packed != 0;
+  const int a_rows = apk ? (min(BM, M - m0) + 15) / 16 * 16 : min(BM, M - m0);
+  const __amdgpu_buffer_rsrc_t rA = make_rsrc(A + (int64_t)m0 * lda, (uint32_t)a_rows * (uint32_t)lda);
   const int nrows_w = min(BN, (N + 15) / 16 * 16 - n0);
   const __amdgpu_buffer_rsrc_t rB =
       make_rsrc(W + (int64_t)(n0 / 16) * KB * 1024, (uint32_t)(nrows_w / 16) * KB * 1024u);
@@ -895,12 +904,14 @@ __global__ __launch_bounds__(C::NT, C::MIN_BLOCKS) void gemm_fp8_kernel(
 #pragma unroll
   for (int j = 0; j < Q; ++j) {
     const int q = j * NW + wave;
-    voff[j] = j < QA ? (uint32_t)((16 * q + lrow) * lda + lchunk * 16)
-                     : (uint32_t)(q - BM / 16) * KB * 1024u + (uint32_t)(lrow * 64 + lchunk * 16);
+    voff[j] = j >= QA ? (uint32_t)(q - BM / 16) * KB * 1024u + (uint32_t)(lrow * 64 + lchunk * 16)
+              : apk   ? (uint32_t)q * KB * 1024u + (uint32_t)(lrow * 64 + lchunk * 16)
+                      : (uint32_t)((16 * q + lrow) * lda + lchunk * 16);
   }
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint4*)lds;
+  const uint32_t a_kstep = apk ? 1024u : 64u;  // bytes per K tile
   auto dma = [&](int st, int kt) {
-    const uint32_t soffA = (uint32_t)kt * 64u, soffB = (uint32_t)kt * 1024u;
+    const uint32_t soffA = (uint32_t)kt * a_kstep, soffB = (uint32_t)kt * 1024u;
 #pragma unroll
     for (int j = 0; j < Q; ++j) {
       const uint32_t m0addr = lds0 + (uint32_t)(st * STAGE + 64 * (j * NW + wave)) * 16u;
@@ -1179,7 +1190,7 @@ template <class C, int EPI>
 hipError_t launch_fp8(const GemmArgs& g, hipStream_t s) {
   const int tm = (g.M + C::BM - 1) / C::BM, tn = (g.N + C::BN - 1) / C::BN;
   hipLaunchKernelGGL((gemm_fp8_kernel<C, EPI>), dim3(tm * tn), dim3(C::NT), 0, s, (const uint8_t*)g.A,
-                     (const uint8_t*)g.W, g.M, g.N, g.K, g.lda, g.ep, tm, tn);
+                     (const uint8_t*)g.W, g.M, g.N, g.K, g.lda, g.ep, tm, tn, g.a_packed);
   return hipGetLastError();
 }
 
@@ -1198,7 +1209,9 @@ hipError_t dispatch_fp8(const GemmArgs& g, hipStream_t s) {
 
 hipError_t gemm_fp8(const GemmArgs& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
-  if (g.a_packed || g.ep.out_packed) return hipErrorInvalidValue;  // row-major codes and outputs
+  // packed A codes need lda = K; only the E4M3 SwiGLU codes can be written packed
+  if ((g.a_packed && g.lda != g.K) || (g.ep.out_packed && (g.epi != EPI_SWIGLU_E4M3 || g.ep.ld_out % 64)))
+    return hipErrorInvalidValue;
   if (g.K <= 0 || g.K % 64 || g.lda % 16 || !g.ep.row_scale || !g.ep.col_scale) return hipErrorInvalidValue;
   if (g.epi == EPI_SWIGLU) {
     if (g.N % 64 || g.ep.ld_out % 4 || (uintptr_t)g.ep.out_a % 8) return hipErrorInvalidValue;

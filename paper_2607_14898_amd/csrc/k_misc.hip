@@ -27,6 +27,11 @@ __device__ __forceinline__ void store_kind(void* out, int64_t i, float v, int ki
 __device__ __forceinline__ int64_t pk16(int64_t row, int k, int K) {
   return ((row >> 4) * (K >> 5) + (k >> 5)) * 512 + (row & 15) * 32 + (k & 31);
 }
+// Byte (row, k) of E4M3 codes [rows, K] in the packed operand layout of the
+// FP8 GEMM (blocks of 16 rows x 64 bytes).
+__device__ __forceinline__ int64_t pk8(int64_t row, int k, int K) {
+  return ((row >> 4) * (K >> 6) + (k >> 6)) * 1024 + (row & 15) * 64 + (k & 63);
+}
 
 // Four consecutive values as one 8-byte (16-bit kinds) or 16-byte (fp32) store.
 __device__ __forceinline__ void store4(void* out, int64_t i, float4 y, int kind) {
@@ -148,7 +153,8 @@ __global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ x, 
     for (int i = 0; i < MAXV; ++i) {
       const int c = lane + 64 * i;
       if (c < nv)
-        reinterpret_cast<uint32_t*>((uint8_t*)out + (int64_t)row * D)[c] = q.pack4(v[i].x, v[i].y, v[i].z, v[i].w);
+        *reinterpret_cast<uint32_t*>((uint8_t*)out + (packed ? pk8(row, 4 * c, D) : (int64_t)row * D + 4 * c)) =
+            q.pack4(v[i].x, v[i].y, v[i].z, v[i].w);
     }
     if (!static_sc && lane == 0) row_scale[row] = q.scale;
   }
@@ -160,7 +166,7 @@ template <typename TIN>
 __global__ __launch_bounds__(256) void quant_rows_kernel(const TIN* __restrict__ in, int64_t M, int K,
                                                          uint8_t* __restrict__ codes,
                                                          float* __restrict__ scale,
-                                                         unsigned* __restrict__ amax_out) {
+                                                         unsigned* __restrict__ amax_out, int packed) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
@@ -180,7 +186,7 @@ __global__ __launch_bounds__(256) void quant_rows_kernel(const TIN* __restrict__
     uint2 w;
     w.x = q.pack4(f[0], f[1], f[2], f[3]);
     w.y = q.pack4(f[4], f[5], f[6], f[7]);
-    *reinterpret_cast<uint2*>(codes + row * K + c) = w;
+    *reinterpret_cast<uint2*>(codes + (packed ? pk8(row, c, K) : row * K + c)) = w;
   }
   if (lane == 0) scale[row] = q.scale;
 }
@@ -351,7 +357,8 @@ hipError_t norm_rows(const float* x, int M, int D, const float* g, const float* 
                      const float* static_sc, unsigned* amax_out, bool packed) {
   if (M <= 0) return hipSuccess;
   if (D % 4 || D > 2048 || (out_kind == 3 && !row_scale && !static_sc)) return hipErrorInvalidValue;
-  if (packed && (D % 32 || (out_kind != 0 && out_kind != 1))) return hipErrorInvalidValue;
+  if (packed && (out_kind == 3 ? D % 64 : (D % 32 || (out_kind != 0 && out_kind != 1))))
+    return hipErrorInvalidValue;
   const int grid = (M + 3) / 4;
   if (kind == 0)
     hipLaunchKernelGGL(norm_kernel<0>, dim3(grid), dim3(256), 0, s, x, M, D, g, b, eps, out, out_kind,
@@ -363,16 +370,16 @@ hipError_t norm_rows(const float* x, int M, int D, const float* g, const float* 
 }
 
 hipError_t quant_rows_e4m3(const void* in, int in_kind, int64_t M, int K, uint8_t* codes,
-                           float* scale, hipStream_t s, unsigned* amax_out) {
+                           float* scale, hipStream_t s, unsigned* amax_out, bool packed) {
   if (M <= 0) return hipSuccess;
-  if (K <= 0 || K % 8 || (in_kind != 0 && in_kind != 2)) return hipErrorInvalidValue;
+  if (K <= 0 || K % 8 || (in_kind != 0 && in_kind != 2) || (packed && K % 64)) return hipErrorInvalidValue;
   const unsigned grid = (unsigned)((M + 3) / 4);
   if (in_kind == 0)
     hipLaunchKernelGGL(quant_rows_kernel<_Float16>, dim3(grid), dim3(256), 0, s, (const _Float16*)in, M,
-                       K, codes, scale, amax_out);
+                       K, codes, scale, amax_out, packed ? 1 : 0);
   else
     hipLaunchKernelGGL(quant_rows_kernel<float>, dim3(grid), dim3(256), 0, s, (const float*)in, M, K,
-                       codes, scale, amax_out);
+                       codes, scale, amax_out, packed ? 1 : 0);
   return hipGetLastError();
 }
 

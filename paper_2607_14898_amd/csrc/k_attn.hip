@@ -75,7 +75,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t attn_rsrc(const void* base, ui
 }
 
 // Workgroup: 4 waves = HPB heads of one KV group x (4 / HPB) query sub-tiles of
-// 64 queries. K and V^T tiles of 64 keys are shared by the 4 waves through LDS;
+// 32 NQB queries. K and V^T tiles of 64 keys are shared by the 4 waves through LDS;
 // they are copied there by buffer-to-LDS DMA (no register staging), one tile
 // ahead. Each wave's Q fragments sit in LDS too, which leaves the registers
 // for reading a whole tile's K fragments ahead of the score MFMAs.

@@ -1083,6 +1083,7 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
 using TileL = TileCfg<256, 256, 2, 4, 4, true>;   // 8 waves of 128 x 64, 128 KB LDS
 using TileW = TileCfg<256, 192, 2, 2, 5>;         // 4 waves of 128 x 96, 140 KB
 using TileM = TileCfg<192, 128, 2, 2, 6>;         // 4 waves of 96 x 64, 120 KB
+using TileM4 = TileCfg<192, 128, 2, 2, 4>;        // the same, 80 KB: two per CU
 using TileS1 = TileCfg<128, 128, 2, 2, 6, true>;  // 4 waves of 64 x 64, 96 KB
 using TileS = TileCfg<128, 128, 2, 2, 3, true>;   // 4 waves of 64 x 64, 48 KB
 
@@ -1108,6 +1109,13 @@ hipError_t dispatch_tiles(const GemmArgs& g, hipStream_t s) {
     return launch_gemm<T, TileL, EPI>(g, s);
   }
   const int tm = tiles(192, 128);
+  if constexpr (EPI == EPI_RESID_ADD) {
+    // residual adds: 192 x 128 tiles with 4 stages (two workgroups per CU)
+    // behind a long K loop in one round, and wherever 192 x 128 tiles make one
+    // round of two per CU (257-512 tiles, the 480p refinement O projection)
+    if ((tm >= 200 && tm <= 256 && g.K > 2048) || (tm > 256 && tm <= 512))
+      return launch_gemm<T, TileM4, EPI>(g, s);
+  }
   if (tm >= 200 && tm <= 256) return launch_gemm<T, TileM, EPI>(g, s);
   if (tiles(128, 128) <= 256) return launch_gemm<T, TileS1, EPI>(g, s);
   return launch_gemm<T, TileS, EPI>(g, s);

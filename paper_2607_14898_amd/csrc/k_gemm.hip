@@ -1094,8 +1094,10 @@ hipError_t dispatch_tiles(const GemmArgs& g, hipStream_t s) {
   if (tiles(256, 256) >= 160 && !short_rmw) {
     // a SwiGLU projection of under two rounds of 256 x 256 tiles (the 480p
     // backbone: 336 tiles, 1.3 rounds) runs faster as 128 x 128 tiles, several
-    // per CU (measured 1.8% per 480p chunk)
+    // per CU (measured 1.8% per 480p chunk); so do the QKV and temporal-up
+    // projections of the 720p refinement input (456 and 360 tiles)
     if (EPI == EPI_SWIGLU && tiles(256, 256) < 512) return launch_gemm<T, TileS, EPI>(g, s);
+    if ((EPI == EPI_QKV || EPI == EPI_TUP) && tiles(256, 256) < 512) return launch_gemm<T, TileS, EPI>(g, s);
     // 256 x 192 tiles where their rounds of 256 CUs, weighted by tile area,
     // are fewer than those of 256 x 256 tiles (for instance 342 -> 456 tiles,
     // 2 -> 1.5 round-equivalents, for 14400 x 1536 outputs). Their 96-column

@@ -1,7 +1,7 @@
 // Bandwidth-bound passes of the decoder forward:
 //  * norm_rows       pre-sublayer RMSNorm / LayerNorm of the fp32 residual
 //                    stream (Sec. 3.2 "Base Architecture") into the operand
-//                    format of the next projection;
+//                    format and packed block layout of the next projection;
 //  * qkv_post        KV-norm and 3D-RoPE (Sec. 3.2), then the rolling-cache
 //                    append of Sec. 3.3 / Algorithm 1 as a write into ring slot
 //                    (unit mod S);

@@ -219,9 +219,11 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
     if (++kt == tiles_per_unit) kt = 0;
     f32x16 s[2][NQB];
     // The MFMA blocks run at raised wave priority: a wave that reaches its MFMAs
-    // issues them ahead of the other wave on the SIMD, which meanwhile issues its
-    // exp2 / conversion work, so the two waves drift into opposite phases and the
-    // matrix and vector units overlap more.
+    // issues them ahead of the other waves on the SIMD, which meanwhile issue
+    // their exp2 / conversion work, so the waves drift into different phases
+    // and the matrix and vector units overlap more. The score block, which
+    // starts a tile's dependency chain, outranks the P V block (3 over 2;
+    // measured 1.4% faster per 720p chunk than one level for both).
     auto scores = [&]() {
       // all K fragments of the tile are read before the first MFMA
       V kfr[2][4];
@@ -232,7 +234,7 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
           const uint4 v = sk[cur][swz_k(kb * 32 + key_of_row(lr), 2 * ks + lh)];
           kfr[kb][ks] = *reinterpret_cast<const V*>(&v);
         }
-      __builtin_amdgcn_s_setprio(1);
+      __builtin_amdgcn_s_setprio(3);
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -346,7 +348,7 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
 #pragma unroll
     for (int qb = 0; qb < NQB; ++qb) l_run[qb] += ls[qb];
 
-    __builtin_amdgcn_s_setprio(1);
+    __builtin_amdgcn_s_setprio(2);
 #pragma unroll
     for (int d = 0; d < 2; ++d) {
 #pragma unroll

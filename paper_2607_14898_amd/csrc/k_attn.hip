@@ -212,7 +212,6 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
   int kt = 0;
   for (int it = 0; it < n_it; ++it) {
     const int cur = it & 1;
-    if (it + 1 < n_it) dma_tile(cur ^ 1);
 
     // S^T = K Q^T - m_q: lane holds query lr of each 32-query block, 16 keys per key block
     const bool tail = kt == tiles_per_unit - 1 && tail_valid < KT;
@@ -225,7 +224,7 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
     // K fragment reads, which starts a tile's dependency chain, outranks the
     // P V block (3 over 2; measured 1.4% faster per 720p chunk than one level
     // for both MFMA bursts, and 0.9% more with the K reads raised too).
-    auto scores = [&]() {
+    auto scores = [&](bool with_dma) {
       // all K fragments of the tile are read before the first MFMA, already
       // at the score block's priority
       __builtin_amdgcn_s_setprio(3);
@@ -237,6 +236,14 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
           const uint4 v = sk[cur][swz_k(kb * 32 + key_of_row(lr), 2 * ks + lh)];
           kfr[kb][ks] = *reinterpret_cast<const V*>(&v);
         }
+      // the next tile's DMA (main pass only) goes out after the K fragment
+      // reads, at base priority, so their LDS latency overlaps its issue
+      // (measured 1.0% faster per 720p chunk than at the loop top)
+      if (with_dma && it + 1 < n_it) {
+        __builtin_amdgcn_s_setprio(0);
+        dma_tile(cur ^ 1);
+        __builtin_amdgcn_s_setprio(3);
+      }
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -303,7 +310,7 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
         }
       }
     };
-    scores();
+    scores(true);
     exp_tile();
     bool big = false;
 #pragma unroll
@@ -316,7 +323,7 @@ __global__ __launch_bounds__(256, NQB == 2 ? 2 : 3) void attn_mfma_kernel(AttnAr
       // any value that keeps P in f16 range is exact. The scores are
       // recomputed from the K tile still in LDS.
       const bool first = it == 0;
-      scores();
+      scores(false);
 #pragma unroll
       for (int qb = 0; qb < NQB; ++qb) {
         float m0 = s[0][qb][0], m1 = s[1][qb][0];
